@@ -1,0 +1,182 @@
+"""Decode-step throughput of the ASR-KF-EGR hot path on one MI355X.
+
+A step is the whole path for every layer and sequence: append, attention over
+the active cache with relevance and the freeze schedule (one launch per layer)
+plus the split combine, then entropy, recovery and the rebuild of every
+active list.  Inputs are synthetic (seeded generator, device twin) and sit in
+HBM before the timed region starts.
+
+Prints one JSON line.  value = attended (active) KV token-layers per second.
+"""
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_HBM_GBS = 8000.0
+WORKLOADS = {"32layer": "llama8b_32layer", "1layer": "llama8b_1layer", "ragged": "ragged"}
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=112)
+    ap.add_argument("--warmup", type=int, default=16)
+    ap.add_argument("--workload", choices=sorted(WORKLOADS), default="32layer")
+    ap.add_argument("--cpu-seconds", type=float, default=15.0,
+                    help="budget of the oracle sample (0 disables the cpu_baseline leg)")
+    ap.add_argument("--traffic-json", default=os.path.join(ROOT, "profiles", "attention_traffic.json"),
+                    help="HBM bytes per launch measured with rocprofv3 counters, if present")
+    return ap.parse_args()
+
+
+def cpu_baseline(w, budget_s):
+    """The CPU oracle on a bounded sample: one (layer, seq) instance, the
+    first steps of the run, until the time budget is spent."""
+    import numpy as np
+    import oracle
+    from synth import gen
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    except Exception:
+        threads = 1
+    P = w.prefill[0]
+    K, V = gen.kv_rows(w, 0, 0, 0, P + w.steps)
+    inst = oracle.Instance(K[:P], V[:P], w.window_K, w.tau, w.k_soft, capacity=P + w.steps + 1)
+    attended, spent, steps = 0, 0.0, 0
+    for t in range(1, w.steps + 1):
+        q = gen.q_row(w, 0, 0, t)
+        t0 = time.perf_counter()
+        rec = inst.step(q, K[P + t - 1], V[P + t - 1])
+        spent += time.perf_counter() - t0
+        attended += len(rec.active)
+        steps = t
+        if spent >= budget_s:
+            break
+    return {"value": attended / spent, "unit": "active KV token-layers/s", "cores": threads,
+            "kind": "oracle",
+            "sample": f"layer 0, sequence 0 of {w.name}: steps 1..{steps} "
+                      f"({attended} attended token-layers in {spent:.1f} s); "
+                      f"the full step has {w.n_layers * w.batch} such instances"}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only: this build has no multi-GPU path "
+              f"(asked for --gpus {args.gpus}).", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    import paper_2512_11221_amd as A
+    from synth import gen
+    from synth.device import DeviceGen
+
+    A.load()
+    torch.cuda.set_device(0)
+    W, K = args.warmup, args.steps
+    w = getattr(gen, WORKLOADS[args.workload])(steps=W + K)
+    L, B, Hq, Hkv, D = w.n_layers, w.batch, w.n_q_heads, w.n_kv_heads, w.head_dim
+    tdt = torch.bfloat16 if w.dtype == "bf16" else torch.float32
+
+    cfg = A.make_config(L, B, Hq, Hkv, D, w.max_ctx, w.window_K, w.tau, w.k_soft, w.vocab,
+                        entropy_spike=w.entropy_spike, conf_drop=w.conf_drop,
+                        wr_last_N=w.wr_last_N, dtype=w.dtype)
+    ctx = A.asrkf_init(cfg)
+    dg = DeviceGen(w)
+    # prompt KV, one (layer, seq) at a time through a staging buffer
+    Pmax = max(w.prefill)
+    stage_k = torch.empty(Pmax * Hkv * D, dtype=tdt, device="cuda")
+    stage_v = torch.empty_like(stage_k)
+    for l in range(L):
+        for b in range(B):
+            P = w.prefill[b]
+            dg.kv_rows(l, b, 0, P, stage_k, stage_v)
+            A.asrkf_prefill(ctx, l, b, stage_k, stage_v, P)
+    del stage_k, stage_v
+    S = W + K
+    Q = torch.empty((S, L, B, Hq, D), dtype=tdt, device="cuda")
+    Kn = torch.empty((S, L, B, Hkv, D), dtype=tdt, device="cuda")
+    Vn = torch.empty_like(Kn)
+    LG = torch.empty((S, B, w.vocab), dtype=torch.float32, device="cuda")
+    dg.q(1, S, Q)
+    dg.new_kv(1, S, Kn, Vn)
+    dg.logits(1, S, LG)
+    out = torch.empty((L, B, Hq, D), dtype=torch.float32, device="cuda")
+    torch.cuda.synchronize()
+
+    def step(t):
+        i = t - 1
+        for l in range(L):
+            A.asrkf_decode_step(ctx, l, Q[i, l], Kn[i, l], Vn[i, l], out[l])
+        A.asrkf_restore(ctx, LG[i], A.AUTO)
+
+    for t in range(1, W + 1):
+        step(t)
+    torch.cuda.synchronize()
+    A.asrkf_stats_reset(ctx)
+    A.asrkf_set_timing(ctx, True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for t in range(W + 1, W + K + 1):
+        step(t)
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    st = A.asrkf_stats(ctx)
+    A.asrkf_destroy(ctx)
+
+    attended = st["attended_total"]
+    bytes_per_token = w.kv_bytes_per_token()          # K + V of one token, one layer
+    algo_bytes = bytes_per_token * attended + 4 * w.vocab * B * K
+    attn_s = st["attn_kernel_ms"] / 1e3
+    achieved = bytes_per_token * attended / attn_s / 1e9
+    traffic = None
+    if os.path.exists(args.traffic_json):
+        with open(args.traffic_json) as f:
+            tj = json.load(f)
+        if tj.get("workload") == w.name:
+            traffic = tj.get("bytes_per_launch")
+    total_positions = sum(p + W + K for p in w.prefill) * L
+    line = {
+        "metric": "active-KV tokens/s per decode step + achieved HBM GB/s vs peak, 8B shape",
+        "value": attended / elapsed,
+        "unit": "active KV token-layers/s",
+        "n_gpus": 1,
+        "steps": K,
+        "warmup": W,
+        "ms_per_step": 1e3 * elapsed / K,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": w.dtype,
+        "data": "synthetic (seeded heavy-hitter generator, device twin)",
+        "config": {"workload": w.name, "layers": L, "batch": B, "context": w.prefill[0]
+                   if len(set(w.prefill)) == 1 else "ragged", "q_heads": Hq, "kv_heads": Hkv,
+                   "head_dim": D, "window_K": w.window_K, "tau": w.tau, "k": w.k_soft,
+                   "vocab": w.vocab, "mode": "resident"},
+        "decode_steps_per_s": K / elapsed,
+        "hbm_fraction_step": algo_bytes / elapsed / 1e9 / PEAK_HBM_GBS,
+        "attended_fraction": attended / max(1, sum(p + t for p in w.prefill
+                                                   for t in range(W + 1, W + K + 1)) * L),
+        "compression_after_run": st["compression"],
+        "roofline": {"bound": "hbm", "achieved": achieved, "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                     "frac": achieved / PEAK_HBM_GBS, "traffic": traffic,
+                     "kernel": "attention_kernel<bf16,128,4>",
+                     "launches": st["attn_launches"],
+                     "avg_launch_us": 1e3 * st["attn_kernel_ms"] / max(1, st["attn_launches"]),
+                     "algorithmic_bytes_per_launch": bytes_per_token * attended
+                     / max(1, st["attn_launches"])},
+    }
+    if args.cpu_seconds > 0:
+        line["cpu_baseline"] = cpu_baseline(w, args.cpu_seconds)
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

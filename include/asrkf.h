@@ -1,0 +1,180 @@
+/*
+ * asrkf.h -- C ABI of the MI355X (gfx950) decode-step library for
+ * Adaptive Soft Rolling KV Freeze with Entropy-Guided Recovery
+ * (arXiv 2512.11221).
+ *
+ * One context holds the KV cache and token states of n_layers x batch
+ * (layer, sequence) instances.  A decode step is
+ *
+ *     for layer in 0 .. n_layers-1:  asrkf_decode_step(ctx, layer, ...)
+ *     asrkf_restore(ctx, logits, mode, stream)
+ *
+ * decode_step is Algorithm 1 up to and including the freeze loop for one
+ * layer of every sequence (attention over the active cache, Eq. 1; relevance,
+ * Eq. 2; freeze schedule, Eq. 3).  restore is the rest of the step: entropy
+ * monitoring and staged recovery (Sec. 3.6), then the timer loop and the
+ * rebuild of every active cache for the next step (Sec. 3.5).
+ *
+ * Conventions for every call:
+ *  - Pointers named "device" must point to GPU memory of the current HIP
+ *    device; "host" pointers to CPU memory.  Arrays are dense, row-major,
+ *    in the layout given per argument.  The caller keeps ownership of every
+ *    buffer it passes and keeps it valid until the work queued on `stream`
+ *    has finished.  The library owns its cache, state, scratch and events.
+ *  - `stream` is a hipStream_t passed as void*; NULL is the default stream.
+ *    Calls marked "asynchronous" only queue work on that stream.
+ *  - On any HIP runtime error the context is poisoned: that call returns
+ *    ASRKF_EHIP and every later call returns ASRKF_ESTATE until destroy.
+ *    asrkf_last_error() gives a message for the calling thread.
+ *  - One host thread per context; calls on one context are not re-entrant.
+ */
+#ifndef ASRKF_H
+#define ASRKF_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    ASRKF_OK = 0,
+    ASRKF_EINVAL = -1,     /* bad argument or configuration; nothing done */
+    ASRKF_ENOMEM = -2,     /* device or pinned host allocation failed */
+    ASRKF_EHIP = -3,       /* HIP runtime error; context poisoned */
+    ASRKF_ESTATE = -4,     /* call out of order, or context poisoned */
+    ASRKF_ECAPACITY = -5   /* a sequence would exceed max_ctx positions */
+} asrkf_status;
+
+typedef enum { ASRKF_BF16 = 0, ASRKF_F32 = 1 } asrkf_dtype;
+
+/* Recovery applied at the end of a step (Sec. 3.6 escalation ladder). */
+typedef enum {
+    ASRKF_AUTO = 0,   /* entropy-driven: level = consecutive spike steps, capped at FR */
+    ASRKF_SR = 1,     /* Soft Reset: restore frozen tokens whose remaining timer > 1 */
+    ASRKF_WR = 2,     /* Window Reset: restore frozen tokens among the last wr_last_N positions */
+    ASRKF_FR = 3,     /* Full Reset: restore every frozen token (counts are kept) */
+    ASRKF_NONE = 4    /* no recovery; entropy is still computed when logits are given */
+} asrkf_recover;
+
+typedef struct {
+    int32_t n_layers;        /* >= 1 */
+    int32_t batch;           /* sequences, 1 .. 1024 */
+    int32_t n_q_heads;       /* H in Eq. 2 */
+    int32_t n_kv_heads;      /* 1 .. 8; n_q_heads / n_kv_heads in {1, 2, 4, 8} */
+    int32_t head_dim;        /* 64 or 128 */
+    int32_t max_ctx;         /* positions per sequence: prompt + decode steps */
+    int32_t window_K;        /* protected window of most recent positions (Sec. 3.2; paper: 32) */
+    float   tau;             /* relevance threshold, strict s_j < tau (paper: 0.5) */
+    float   k_soft;          /* Eq. 3 softness k, in [2^-8, 2^16] (paper: 2) */
+    int32_t vocab;           /* logits per sequence for entropy; >= 1 */
+    float   entropy_spike;   /* theta_H in nats; +inf disables the entropy trigger */
+    float   conf_drop;       /* theta_p on the top probability; <= 0 disables */
+    int32_t wr_last_N;       /* Window Reset span in positions; <= 0 means 4 * window_K */
+    asrkf_dtype dtype;       /* storage type of q, k, v */
+    int32_t spill_min_D;     /* 0: frozen KV stays in HBM (resident mode) */
+} asrkf_config;
+
+typedef struct {
+    int64_t step;               /* completed decode steps t */
+    int64_t total_positions;    /* sum over (layer, seq) of positions n_t */
+    int64_t active_positions;   /* sum over (layer, seq) of |{p < n_t : active at t+1}|
+                                   -- the "Active KV" column of Table 1 */
+    int64_t attended_total;     /* sum over completed steps and (layer, seq) of |A_t| */
+    int64_t recoveries[4];      /* [1] SR, [2] WR, [3] FR applications (per sequence) */
+    int64_t rr_requests;        /* steps at which the ladder asked for Rewalk Regeneration */
+    int64_t attn_launches;      /* timed attention launches (asrkf_set_timing) */
+    double  attn_kernel_ms;     /* summed duration of those launches */
+    double  compression;        /* 1 - active_positions / total_positions */
+} asrkf_stats_t;
+
+typedef struct asrkf_ctx asrkf_ctx;
+
+/* Allocate the cache and token states of every (layer, sequence): the
+ * active cache A, frozen storage F and states S of Algorithm 1 (REQUIRE).
+ * cfg: host.  On success *out receives the context.  Errors: EINVAL for a
+ * configuration outside the documented ranges, ENOMEM, EHIP. */
+asrkf_status asrkf_init(const asrkf_config* cfg, asrkf_ctx** out);
+
+/* Copy the prompt KV of one (layer, sequence) into the cache (Sec. 3.1: the
+ * pairs (K_j, V_j) of every previous token).  k, v: device,
+ * [n_tokens][n_kv_heads][head_dim] of cfg.dtype.  Every layer of a sequence
+ * must be given the same n_tokens (1 .. max_ctx-1); a sequence never
+ * prefilled starts empty.  Only before the first decode step (else ESTATE).
+ * Asynchronous. */
+asrkf_status asrkf_prefill(asrkf_ctx* ctx, int32_t layer, int32_t seq,
+                           const void* k, const void* v, int32_t n_tokens, void* stream);
+
+/* Algorithm 1 up to the end of the freeze loop, for one layer of every
+ * sequence: append the new token, attend over the active cache (Eq. 1),
+ * score every attended token (Eq. 2), and freeze low-relevance tokens outside
+ * the window of the window_K most recent positions (Eq. 3).
+ *   q:     device, [batch][n_q_heads][head_dim] of cfg.dtype
+ *   k_new: device, [batch][n_kv_heads][head_dim] of cfg.dtype
+ *   v_new: device, same layout as k_new
+ *   out:   device, [batch][n_q_heads][head_dim] float32 (written)
+ * Layers must come in order 0 .. n_layers-1 within a step (else ESTATE);
+ * ECAPACITY when a sequence has no room for the new position.  Asynchronous. */
+asrkf_status asrkf_decode_step(asrkf_ctx* ctx, int32_t layer, const void* q,
+                               const void* k_new, const void* v_new, float* out,
+                               void* stream);
+
+/* End the step: entropy of each sequence's next-token distribution and the
+ * recovery ladder (Sec. 3.6), then the timer loop and the active caches of
+ * the next step (Algorithm 1 timer loop; Sec. 3.5).
+ *   logits: device, [batch][vocab] float32, or NULL (no entropy; AUTO then
+ *           applies no recovery)
+ *   mode:   see asrkf_recover; a forced level applies to every sequence.
+ * Must follow decode_step of the last layer (else ESTATE).  Asynchronous. */
+asrkf_status asrkf_restore(asrkf_ctx* ctx, const float* logits, asrkf_recover mode,
+                           void* stream);
+
+/* Counters of the context (Table 1 columns, attended tokens, recoveries).
+ * out: host.  Waits for all queued work of the context. */
+asrkf_status asrkf_stats(asrkf_ctx* ctx, asrkf_stats_t* out);
+
+/* Zero the cumulative counters (attended_total, recoveries, rr_requests,
+ * attention timing).  Waits for all queued work of the context. */
+asrkf_status asrkf_stats_reset(asrkf_ctx* ctx);
+
+/* Record HIP events around every attention launch (enable != 0) so that
+ * asrkf_stats reports the kernel's summed duration.  Host-side switch. */
+asrkf_status asrkf_set_timing(asrkf_ctx* ctx, int32_t enable);
+
+/* Token states of one (layer, sequence) after the last completed step t
+ * (test export).  All outputs are host buffers of at least max_ctx entries
+ * (any may be NULL):
+ *   n_positions:   receives n_t
+ *   unfreeze_step: [n_t] step at which a frozen token attends again
+ *                  (a token attends at step t' iff its value is <= t')
+ *   count:         [n_t] low-relevance detections c_j (Eq. 3)
+ *   frozen:        [n_t] 1 if the token is excluded at step t+1
+ *   active:        ascending positions attended at step t+1 (including the
+ *                  position the next token will take); *n_active their number
+ * Waits for all queued work of the context. */
+asrkf_status asrkf_get_state(asrkf_ctx* ctx, int32_t layer, int32_t seq,
+                             int32_t* n_positions, int32_t* unfreeze_step, int32_t* count,
+                             uint8_t* frozen, int32_t* active, int32_t* n_active);
+
+/* Entropy monitor of one sequence after the last restore (Sec. 3.6):
+ * entropy (nats), top probability, consecutive spike steps, level applied.
+ * Host outputs, any may be NULL.  Waits for all queued work. */
+asrkf_status asrkf_get_seq(asrkf_ctx* ctx, int32_t seq, float* entropy, float* pmax,
+                           int32_t* escalation, int32_t* level);
+
+/* Host-only helper: d(c) = floor(sqrt(c) / k) of Eq. 3 for c = 0 .. n-1,
+ * exact for the float32 value k_soft (the table the library uses).
+ * out: host, n entries.  EINVAL if k_soft is outside [2^-8, 2^16] or n < 1. */
+asrkf_status asrkf_schedule_table(float k_soft, int32_t n, int32_t* out);
+
+/* Free everything the context owns.  Waits for its queued work.  NULL is a no-op. */
+void asrkf_destroy(asrkf_ctx* ctx);
+
+/* Message of the last failed call on this thread ("" if none). */
+const char* asrkf_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* ASRKF_H */

@@ -1,0 +1,42 @@
+"""Build libasrkf.so (the HIP kernels + C ABI) for gfx950 with hipcc, in-tree."""
+import os
+import shutil
+import subprocess
+import tempfile
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+CSRC = os.path.join(HERE, "csrc")
+LIB = os.path.join(HERE, "libasrkf.so")
+SOURCES = ["attention.hip", "compact.hip", "entropy.hip", "runtime.hip"]
+ARCH = "gfx950"
+# no packed fp32 instructions anywhere in the device code
+DEVICE_FLAGS = ["-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"]
+
+
+def hipcc():
+    for cand in (os.environ.get("HIPCC"), "/opt/rocm/bin/hipcc", shutil.which("hipcc")):
+        if cand and os.path.exists(cand):
+            return cand
+    raise RuntimeError("hipcc not found")
+
+
+def compile_shared(sources, out, extra=(), cwd=None):
+    fd, tmp = tempfile.mkstemp(suffix=".so", dir=os.path.dirname(out))
+    os.close(fd)
+    cmd = [hipcc(), f"--offload-arch={ARCH}", "-O3", "-std=c++17", "-fPIC", "-shared",
+           *DEVICE_FLAGS, *extra, *sources, "-o", tmp]
+    try:
+        subprocess.run(cmd, check=True, cwd=cwd, stdout=subprocess.PIPE, stderr=subprocess.STDOUT)
+    except subprocess.CalledProcessError as e:
+        os.unlink(tmp)
+        raise RuntimeError("hipcc failed:\n" + " ".join(cmd) + "\n" + e.stdout.decode(errors="replace"))
+    os.replace(tmp, out)
+    return out
+
+
+def build():
+    return compile_shared([os.path.join(CSRC, s) for s in SOURCES], LIB)
+
+
+if __name__ == "__main__":
+    print(build())

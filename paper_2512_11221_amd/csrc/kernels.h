@@ -1,0 +1,84 @@
+// Internal interface between the runtime (runtime.hip) and the kernels.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace asrkf {
+
+// Split-K attention: the active lists of all sequences, concatenated, are cut
+// into one contiguous range per workgroup of a fixed grid; every workgroup
+// derives the cut from the active counts on the device (no host round trip).
+// A range is walked in chunks of at most kChunkMax tokens (LDS staging).
+constexpr int kChunkMax = 1024;
+constexpr int kMaxBatch = 1024;
+
+struct AttnArgs {
+    const void* kpool;        // layer base, [B][cap][Hkv][D]
+    const void* vpool;
+    const void* q;            // [B][Hq][D]
+    const void* knew;         // [B][Hkv][D]
+    const void* vnew;
+    void* kpool_w;            // same as kpool, writable (append)
+    void* vpool_w;
+    const int32_t* list;      // layer base, [B][cap] ascending positions
+    const int32_t* n_active;  // layer base, [B]
+    const int32_t* plen;      // [B] prompt length
+    int32_t* unfreeze;        // layer base, [B][cap]: U_j
+    int32_t* count;           // layer base, [B][cap]: c_j
+    const int32_t* dur;       // [dur_len] freeze duration by count (Eq. 3)
+    float* part_acc;          // [grid + B][Hq][D]: partial of (workgroup w, seq b) at slot w + b
+    float* part_ml;           // [grid + B][Hq][2]: (max in log2 units, sum)
+    int32_t* slot_first;      // [B] first partial slot of each sequence (written)
+    int32_t* slot_end;        // [B] one past its last slot (written)
+    int32_t B, cap, Hq, Hkv;
+    int32_t t;                // current step (1-based)
+    int32_t window_K;
+    int32_t dur_len;
+    float tau_H;              // tau * Hq: compared against sum_h |q_h . k_j|
+    float scale_log2;         // log2(e) / sqrt(D)
+};
+
+struct CombineArgs {
+    const float* part_acc;
+    const float* part_ml;
+    const int32_t* slot_first;
+    const int32_t* slot_end;
+    float* out;               // [B][Hq][D]
+    int32_t B, Hq;
+};
+
+struct CompactArgs {
+    int32_t* unfreeze;        // [L][B][cap]
+    int32_t* list;            // [L][B][cap]
+    int32_t* n_active;        // [L][B]
+    const int32_t* plen;      // [B]
+    const int32_t* level;     // [B] recovery level per sequence (may be null)
+    unsigned long long* listed_total;  // running sum of list lengths
+    int32_t forced_level;     // -1: read level[]; 0: none; 1..3 forced SR/WR/FR
+    int32_t t;                // completed step; lists are built for step t+1
+    int32_t B, cap, wr_last_N;
+};
+
+struct EntropyArgs {
+    const float* logits;      // [B][V]
+    int32_t V, B;
+    float theta_H, theta_p;
+    int32_t mode;             // 0 AUTO, 1..3 forced, 4 none
+    int32_t* escalation;      // [B]
+    int32_t* level;           // [B] (written)
+    float* entropy;           // [B]
+    float* pmax;              // [B]
+    unsigned long long* recoveries;  // [4], indexed by level 1..3
+    unsigned long long* rr_requests;
+};
+
+hipError_t launch_attention(const AttnArgs& a, int dtype_bf16, int head_dim, int group,
+                            int grid, hipStream_t s);
+hipError_t attention_occupancy(const AttnArgs& a, int dtype_bf16, int head_dim, int group,
+                               int* blocks_per_cu);
+hipError_t launch_combine(const CombineArgs& a, int head_dim, hipStream_t s);
+hipError_t launch_compact(const CompactArgs& a, int n_instances, hipStream_t s);
+hipError_t launch_entropy(const EntropyArgs& a, hipStream_t s);
+
+}  // namespace asrkf

@@ -1,0 +1,587 @@
+// Context, memory layout and the C ABI declared in include/asrkf.h.
+//
+// HBM layout of a context (cap = max_ctx + 1 rounded up to 64 positions):
+//   K, V cache      [L][B][cap][Hkv][D]   dtype   token-major rows
+//   unfreeze U      [L][B][cap]           int32   token attends at step t iff U <= t
+//   count c         [L][B][cap]           int32   low-relevance detections (Eq. 3)
+//   active list     [L][B][cap]           int32   ascending positions for the step
+//   n_active        [L][B]                int32
+//   partials        [grid+B][Hq][D+2]     fp32    split-K attention partials
+//   per sequence    prompt length, escalation, level, entropy, p_max
+//   duration table  [max_ctx + 2]         int32   d(c) of Eq. 3, built exactly on the host
+#include <math.h>
+#include <stdarg.h>
+#include <stdio.h>
+#include <string.h>
+
+#include <algorithm>
+#include <string>
+#include <utility>
+#include <vector>
+
+#include "../../include/asrkf.h"
+#include "kernels.h"
+
+using namespace asrkf;
+
+namespace {
+
+thread_local std::string g_last_error;
+
+asrkf_status fail(asrkf_status st, const char* fmt, ...) {
+    char buf[512];
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(buf, sizeof buf, fmt, ap);
+    va_end(ap);
+    g_last_error = buf;
+    return st;
+}
+
+// d(c) = floor(sqrt(c) / k) for the exact binary value of k: the largest
+// integer d with (d k)^2 <= c.  k = M 2^E with M < 2^24 an integer.
+int32_t exact_duration(uint64_t c, float k) {
+    int e2;
+    const float fr = frexpf(k, &e2);                  // k = fr * 2^e2, fr in [0.5, 1)
+    const uint64_t M = (uint64_t)ldexpf(fr, 24);      // exact 24-bit mantissa
+    const int E = e2 - 24;                            // k = M * 2^E
+    // test (d M)^2 2^(2E) <= c  <=>  (d M)^2 <= c 2^(-2E)   (E < 0)
+    //                           <=>  (d M)^2 2^(2E) <= c     (E >= 0)
+    auto fits = [&](uint64_t d) -> bool {
+        const unsigned __int128 lhs = (unsigned __int128)(d * M) * (d * M);
+        if (E >= 0) {
+            if (2 * E >= 100) return d == 0;
+            return (lhs << (2 * E)) <= (unsigned __int128)c;
+        }
+        return lhs <= ((unsigned __int128)c << (-2 * E));
+    };
+    // initial guess from floating point, then fix up exactly
+    double g = floor(sqrt((double)c) / (double)k);
+    uint64_t d = g > 0 ? (uint64_t)g : 0;
+    while (d > 0 && !fits(d)) --d;
+    while (fits(d + 1)) ++d;
+    return (int32_t)d;
+}
+
+bool valid_k(float k) { return isfinite(k) && k >= 0x1p-8f && k <= 0x1p16f; }
+
+}  // namespace
+
+struct asrkf_ctx {
+    asrkf_config cfg{};
+    int cap = 0;                 // positions per (layer, seq) array
+    int group = 0;
+    size_t esz = 0;
+    size_t row_bytes = 0;        // one token, all KV heads
+    int grid = 0;                // persistent attention grid (resident workgroups)
+    int n_slots = 0;             // partial slots: grid + batch
+    int dur_len = 0;
+
+    // device memory
+    void* kpool = nullptr;
+    void* vpool = nullptr;
+    int32_t* unfreeze = nullptr;
+    int32_t* count = nullptr;
+    int32_t* list = nullptr;
+    int32_t* n_active = nullptr;
+    int32_t* plen = nullptr;
+    int32_t* dur = nullptr;
+    int32_t* escalation = nullptr;
+    int32_t* level = nullptr;
+    float* entropy = nullptr;
+    float* pmax = nullptr;
+    float* part_acc = nullptr;
+    float* part_ml = nullptr;
+    int32_t* slot_info = nullptr;   // [2B]: first slot, end slot per sequence
+    unsigned long long* counters = nullptr;   // [0] listed_total, [1..3] recoveries, [5] rr
+
+    std::vector<int32_t> plen_host;
+    std::vector<char> prefilled;   // per sequence
+    int t = 0;                     // completed steps
+    int next_layer = 0;            // next layer expected by decode_step
+    bool lists_ready = false;
+    bool poisoned = false;
+    bool timing = false;
+    hipStream_t last_stream = nullptr;
+    std::vector<std::pair<hipEvent_t, hipEvent_t>> ev_used, ev_free;
+    double attn_ms_done = 0.0;
+    int64_t attn_launches = 0;
+    int64_t host_recoveries[4] = {0, 0, 0, 0};
+    int device = 0;
+};
+
+namespace {
+
+asrkf_status hip_fail(asrkf_ctx* ctx, hipError_t e, const char* what) {
+    if (ctx) ctx->poisoned = true;
+    return fail(ASRKF_EHIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+#define HIP_OK(ctx, expr)                                              \
+    do {                                                               \
+        hipError_t e_ = (expr);                                        \
+        if (e_ != hipSuccess) return hip_fail((ctx), e_, #expr);       \
+    } while (0)
+
+asrkf_status check_ctx(asrkf_ctx* ctx) {
+    if (!ctx) return fail(ASRKF_EINVAL, "null context");
+    if (ctx->poisoned) return fail(ASRKF_ESTATE, "context poisoned by an earlier HIP error");
+    return ASRKF_OK;
+}
+
+template <typename T>
+asrkf_status dev_alloc(asrkf_ctx* ctx, T** p, size_t bytes) {
+    void* q = nullptr;
+    hipError_t e = hipMalloc(&q, bytes ? bytes : 16);
+    if (e != hipSuccess) {
+        (void)hipGetLastError();
+        return fail(ASRKF_ENOMEM, "hipMalloc of %zu bytes failed: %s", bytes, hipGetErrorString(e));
+    }
+    *p = static_cast<T*>(q);
+    (void)ctx;
+    return ASRKF_OK;
+}
+
+void free_all(asrkf_ctx* ctx) {
+    void* ptrs[] = {ctx->kpool, ctx->vpool, ctx->unfreeze, ctx->count, ctx->list,
+                    ctx->n_active, ctx->plen, ctx->dur, ctx->escalation, ctx->level,
+                    ctx->entropy, ctx->pmax, ctx->part_acc, ctx->part_ml, ctx->slot_info,
+                    ctx->counters};
+    for (void* p : ptrs) if (p) (void)hipFree(p);
+    for (auto& ev : ctx->ev_used) { (void)hipEventDestroy(ev.first); (void)hipEventDestroy(ev.second); }
+    for (auto& ev : ctx->ev_free) { (void)hipEventDestroy(ev.first); (void)hipEventDestroy(ev.second); }
+}
+
+asrkf_status validate(const asrkf_config* c) {
+    if (!c) return fail(ASRKF_EINVAL, "null config");
+    if (c->n_layers < 1) return fail(ASRKF_EINVAL, "n_layers must be >= 1");
+    if (c->batch < 1 || c->batch > kMaxBatch) return fail(ASRKF_EINVAL, "batch must be in 1..%d", kMaxBatch);
+    if (c->n_kv_heads < 1 || c->n_kv_heads > 8) return fail(ASRKF_EINVAL, "n_kv_heads must be in 1..8");
+    if (c->n_q_heads < c->n_kv_heads || c->n_q_heads % c->n_kv_heads)
+        return fail(ASRKF_EINVAL, "n_q_heads must be a multiple of n_kv_heads");
+    const int g = c->n_q_heads / c->n_kv_heads;
+    if (g != 1 && g != 2 && g != 4 && g != 8) return fail(ASRKF_EINVAL, "n_q_heads / n_kv_heads must be 1, 2, 4 or 8");
+    if (c->head_dim != 64 && c->head_dim != 128) return fail(ASRKF_EINVAL, "head_dim must be 64 or 128");
+    if (c->max_ctx < 2 || c->max_ctx > (1 << 28)) return fail(ASRKF_EINVAL, "max_ctx must be in 2..2^28");
+    if (c->window_K < 0) return fail(ASRKF_EINVAL, "window_K must be >= 0");
+    if (isnan(c->tau)) return fail(ASRKF_EINVAL, "tau is NaN");
+    if (!valid_k(c->k_soft)) return fail(ASRKF_EINVAL, "k_soft must be in [2^-8, 2^16]");
+    if (c->vocab < 1) return fail(ASRKF_EINVAL, "vocab must be >= 1");
+    if (isnan(c->entropy_spike) || isnan(c->conf_drop)) return fail(ASRKF_EINVAL, "NaN threshold");
+    if (c->dtype != ASRKF_BF16 && c->dtype != ASRKF_F32) return fail(ASRKF_EINVAL, "unknown dtype");
+    if (c->spill_min_D != 0) return fail(ASRKF_EINVAL, "spill mode is not available in this build");
+    return ASRKF_OK;
+}
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15) == 0; }
+
+}  // namespace
+
+extern "C" {
+
+const char* asrkf_last_error(void) { return g_last_error.c_str(); }
+
+asrkf_status asrkf_schedule_table(float k_soft, int32_t n, int32_t* out) {
+    if (!valid_k(k_soft)) return fail(ASRKF_EINVAL, "k_soft must be in [2^-8, 2^16]");
+    if (n < 1 || !out) return fail(ASRKF_EINVAL, "bad table size or null output");
+    for (int32_t c = 0; c < n; ++c) out[c] = exact_duration((uint64_t)c, k_soft);
+    return ASRKF_OK;
+}
+
+asrkf_status asrkf_init(const asrkf_config* cfg, asrkf_ctx** out) {
+    if (!out) return fail(ASRKF_EINVAL, "null output pointer");
+    *out = nullptr;
+    asrkf_status st = validate(cfg);
+    if (st != ASRKF_OK) return st;
+
+    asrkf_ctx* ctx = new asrkf_ctx();
+    ctx->cfg = *cfg;
+    if (ctx->cfg.wr_last_N <= 0) ctx->cfg.wr_last_N = 4 * ctx->cfg.window_K;
+    const asrkf_config& c = ctx->cfg;
+    ctx->cap = (c.max_ctx + 1 + 63) / 64 * 64;
+    ctx->group = c.n_q_heads / c.n_kv_heads;
+    ctx->esz = c.dtype == ASRKF_BF16 ? 2 : 4;
+    ctx->row_bytes = (size_t)c.n_kv_heads * c.head_dim * ctx->esz;
+    ctx->plen_host.assign(c.batch, 0);
+    ctx->prefilled.assign(c.batch, 0);
+
+    hipError_t e = hipGetDevice(&ctx->device);
+    if (e != hipSuccess) { delete ctx; return hip_fail(nullptr, e, "hipGetDevice"); }
+    hipDeviceProp_t prop;
+    e = hipGetDeviceProperties(&prop, ctx->device);
+    if (e != hipSuccess) { delete ctx; return hip_fail(nullptr, e, "hipGetDeviceProperties"); }
+    // persistent grid: as many attention workgroups as can be resident at once
+    {
+        AttnArgs probe{};
+        probe.B = c.batch;
+        probe.Hkv = c.n_kv_heads;
+        int per_cu = 0;
+        e = attention_occupancy(probe, c.dtype == ASRKF_BF16, c.head_dim, ctx->group, &per_cu);
+        if (e != hipSuccess) { delete ctx; return hip_fail(nullptr, e, "hipOccupancyMaxActiveBlocksPerMultiprocessor"); }
+        ctx->grid = std::max(1, per_cu) * prop.multiProcessorCount;
+    }
+    ctx->n_slots = ctx->grid + c.batch;
+    ctx->dur_len = c.max_ctx + 2;
+
+    const size_t inst = (size_t)c.n_layers * c.batch;
+    const size_t per_pos = inst * ctx->cap;
+#define ALLOC(field, bytes)                                       \
+    do {                                                          \
+        st = dev_alloc(ctx, &ctx->field, (bytes));                \
+        if (st != ASRKF_OK) { free_all(ctx); delete ctx; return st; } \
+    } while (0)
+    ALLOC(kpool, per_pos * ctx->row_bytes);
+    ALLOC(vpool, per_pos * ctx->row_bytes);
+    ALLOC(unfreeze, per_pos * 4);
+    ALLOC(count, per_pos * 4);
+    ALLOC(list, per_pos * 4);
+    ALLOC(n_active, inst * 4);
+    ALLOC(plen, (size_t)c.batch * 4);
+    ALLOC(dur, (size_t)ctx->dur_len * 4);
+    ALLOC(escalation, (size_t)c.batch * 4);
+    ALLOC(level, (size_t)c.batch * 4);
+    ALLOC(entropy, (size_t)c.batch * 4);
+    ALLOC(pmax, (size_t)c.batch * 4);
+    ALLOC(part_acc, (size_t)ctx->n_slots * c.n_q_heads * c.head_dim * 4);
+    ALLOC(part_ml, (size_t)ctx->n_slots * c.n_q_heads * 2 * 4);
+    ALLOC(slot_info, (size_t)c.batch * 2 * 4);
+    ALLOC(counters, 8 * sizeof(unsigned long long));
+#undef ALLOC
+
+    std::vector<int32_t> table(ctx->dur_len);
+    for (int i = 0; i < ctx->dur_len; ++i) table[i] = exact_duration((uint64_t)i, c.k_soft);
+#define INIT(expr)                                                              \
+    do {                                                                        \
+        hipError_t e_ = (expr);                                                 \
+        if (e_ != hipSuccess) { st = hip_fail(nullptr, e_, #expr); free_all(ctx); delete ctx; return st; } \
+    } while (0)
+    INIT(hipMemset(ctx->unfreeze, 0, per_pos * 4));
+    INIT(hipMemset(ctx->count, 0, per_pos * 4));
+    INIT(hipMemset(ctx->n_active, 0, inst * 4));
+    INIT(hipMemset(ctx->plen, 0, (size_t)c.batch * 4));
+    INIT(hipMemset(ctx->escalation, 0, (size_t)c.batch * 4));
+    INIT(hipMemset(ctx->level, 0, (size_t)c.batch * 4));
+    INIT(hipMemset(ctx->entropy, 0, (size_t)c.batch * 4));
+    INIT(hipMemset(ctx->pmax, 0, (size_t)c.batch * 4));
+    INIT(hipMemset(ctx->counters, 0, 8 * sizeof(unsigned long long)));
+    INIT(hipMemcpy(ctx->dur, table.data(), table.size() * 4, hipMemcpyHostToDevice));
+    INIT(hipDeviceSynchronize());
+#undef INIT
+    *out = ctx;
+    return ASRKF_OK;
+}
+
+asrkf_status asrkf_prefill(asrkf_ctx* ctx, int32_t layer, int32_t seq, const void* k,
+                           const void* v, int32_t n_tokens, void* stream) {
+    asrkf_status st = check_ctx(ctx);
+    if (st != ASRKF_OK) return st;
+    const asrkf_config& c = ctx->cfg;
+    if (ctx->t > 0 || ctx->next_layer != 0 || ctx->lists_ready)
+        return fail(ASRKF_ESTATE, "prefill after the first decode step");
+    if (layer < 0 || layer >= c.n_layers || seq < 0 || seq >= c.batch)
+        return fail(ASRKF_EINVAL, "layer or sequence out of range");
+    if (n_tokens < 1 || n_tokens > c.max_ctx - 1)
+        return fail(ASRKF_EINVAL, "n_tokens must be in 1..max_ctx-1");
+    if (!k || !v) return fail(ASRKF_EINVAL, "null k or v");
+    if (ctx->prefilled[seq] && ctx->plen_host[seq] != n_tokens)
+        return fail(ASRKF_EINVAL, "sequence %d was prefilled with %d tokens in another layer",
+                    seq, ctx->plen_host[seq]);
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    const size_t off = ((size_t)layer * c.batch + seq) * ctx->cap * ctx->row_bytes;
+    const size_t bytes = (size_t)n_tokens * ctx->row_bytes;
+    HIP_OK(ctx, hipMemcpyAsync((char*)ctx->kpool + off, k, bytes, hipMemcpyDeviceToDevice, s));
+    HIP_OK(ctx, hipMemcpyAsync((char*)ctx->vpool + off, v, bytes, hipMemcpyDeviceToDevice, s));
+    if (!ctx->prefilled[seq]) {
+        ctx->prefilled[seq] = 1;
+        ctx->plen_host[seq] = n_tokens;
+        HIP_OK(ctx, hipMemcpyAsync(ctx->plen + seq, &ctx->plen_host[seq], 4,
+                                   hipMemcpyHostToDevice, s));
+    }
+    ctx->last_stream = s;
+    return ASRKF_OK;
+}
+
+namespace {
+
+asrkf_status build_lists(asrkf_ctx* ctx, int forced_level, hipStream_t s) {
+    CompactArgs a{};
+    a.unfreeze = ctx->unfreeze;
+    a.list = ctx->list;
+    a.n_active = ctx->n_active;
+    a.plen = ctx->plen;
+    a.level = ctx->level;
+    a.listed_total = ctx->counters;
+    a.forced_level = forced_level;
+    a.t = ctx->t;
+    a.B = ctx->cfg.batch;
+    a.cap = ctx->cap;
+    a.wr_last_N = ctx->cfg.wr_last_N;
+    HIP_OK(ctx, launch_compact(a, ctx->cfg.n_layers * ctx->cfg.batch, s));
+    return ASRKF_OK;
+}
+
+}  // namespace
+
+asrkf_status asrkf_decode_step(asrkf_ctx* ctx, int32_t layer, const void* q, const void* k_new,
+                               const void* v_new, float* out, void* stream) {
+    asrkf_status st = check_ctx(ctx);
+    if (st != ASRKF_OK) return st;
+    const asrkf_config& c = ctx->cfg;
+    if (layer != ctx->next_layer)
+        return fail(ASRKF_ESTATE, "decode_step expected layer %d, got %d", ctx->next_layer, layer);
+    if (!q || !k_new || !v_new || !out) return fail(ASRKF_EINVAL, "null argument");
+    if (!aligned16(q) || !aligned16(k_new) || !aligned16(v_new) || !aligned16(out))
+        return fail(ASRKF_EINVAL, "q, k_new, v_new and out must be 16-byte aligned");
+    const int t = ctx->t + 1;
+    for (int b = 0; b < c.batch; ++b)
+        if (ctx->plen_host[b] + t > c.max_ctx)
+            return fail(ASRKF_ECAPACITY, "sequence %d would exceed max_ctx=%d", b, c.max_ctx);
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    if (!ctx->lists_ready) {
+        st = build_lists(ctx, 0, s);          // step 1 attends every prompt position
+        if (st != ASRKF_OK) return st;
+        ctx->lists_ready = true;
+    }
+
+    const size_t inst0 = (size_t)layer * c.batch;
+    AttnArgs a{};
+    const size_t pool_off = inst0 * ctx->cap * ctx->row_bytes;
+    a.kpool = (const char*)ctx->kpool + pool_off;
+    a.vpool = (const char*)ctx->vpool + pool_off;
+    a.kpool_w = (char*)ctx->kpool + pool_off;
+    a.vpool_w = (char*)ctx->vpool + pool_off;
+    a.q = q;
+    a.knew = k_new;
+    a.vnew = v_new;
+    a.list = ctx->list + inst0 * ctx->cap;
+    a.n_active = ctx->n_active + inst0;
+    a.plen = ctx->plen;
+    a.unfreeze = ctx->unfreeze + inst0 * ctx->cap;
+    a.count = ctx->count + inst0 * ctx->cap;
+    a.dur = ctx->dur;
+    a.part_acc = ctx->part_acc;
+    a.part_ml = ctx->part_ml;
+    a.slot_first = ctx->slot_info;
+    a.slot_end = ctx->slot_info + c.batch;
+    a.B = c.batch;
+    a.cap = ctx->cap;
+    a.Hq = c.n_q_heads;
+    a.Hkv = c.n_kv_heads;
+    a.t = t;
+    a.window_K = c.window_K;
+    a.dur_len = ctx->dur_len;
+    a.tau_H = c.tau * (float)c.n_q_heads;
+    a.scale_log2 = (float)(1.4426950408889634 / sqrt((double)c.head_dim));
+
+    std::pair<hipEvent_t, hipEvent_t> ev{nullptr, nullptr};
+    if (ctx->timing) {
+        if (!ctx->ev_free.empty()) {
+            ev = ctx->ev_free.back();
+            ctx->ev_free.pop_back();
+        } else {
+            HIP_OK(ctx, hipEventCreate(&ev.first));
+            HIP_OK(ctx, hipEventCreate(&ev.second));
+        }
+        HIP_OK(ctx, hipEventRecord(ev.first, s));
+    }
+    HIP_OK(ctx, launch_attention(a, c.dtype == ASRKF_BF16, c.head_dim, ctx->group, ctx->grid, s));
+    if (ctx->timing) {
+        HIP_OK(ctx, hipEventRecord(ev.second, s));
+        ctx->ev_used.push_back(ev);
+    }
+
+    CombineArgs cb{};
+    cb.part_acc = ctx->part_acc;
+    cb.part_ml = ctx->part_ml;
+    cb.slot_first = ctx->slot_info;
+    cb.slot_end = ctx->slot_info + c.batch;
+    cb.out = out;
+    cb.B = c.batch;
+    cb.Hq = c.n_q_heads;
+    HIP_OK(ctx, launch_combine(cb, c.head_dim, s));
+
+    ctx->next_layer = layer + 1;
+    ctx->last_stream = s;
+    return ASRKF_OK;
+}
+
+asrkf_status asrkf_restore(asrkf_ctx* ctx, const float* logits, asrkf_recover mode, void* stream) {
+    asrkf_status st = check_ctx(ctx);
+    if (st != ASRKF_OK) return st;
+    const asrkf_config& c = ctx->cfg;
+    if (ctx->next_layer != c.n_layers)
+        return fail(ASRKF_ESTATE, "restore before decode_step of every layer (next layer %d of %d)",
+                    ctx->next_layer, c.n_layers);
+    if ((int)mode < ASRKF_AUTO || (int)mode > ASRKF_NONE) return fail(ASRKF_EINVAL, "unknown recovery mode");
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    int forced;
+    if (logits) {
+        EntropyArgs e{};
+        e.logits = logits;
+        e.V = c.vocab;
+        e.B = c.batch;
+        e.theta_H = c.entropy_spike;
+        e.theta_p = c.conf_drop;
+        e.mode = (int)mode;
+        e.escalation = ctx->escalation;
+        e.level = ctx->level;
+        e.entropy = ctx->entropy;
+        e.pmax = ctx->pmax;
+        e.recoveries = ctx->counters;       // [level] for level 1..3
+        e.rr_requests = ctx->counters + 5;
+        HIP_OK(ctx, launch_entropy(e, s));
+        forced = -1;                           // level[] written by the entropy kernel
+    } else {
+        forced = (mode >= ASRKF_SR && mode <= ASRKF_FR) ? (int)mode : 0;
+        if (forced) ctx->host_recoveries[forced] += c.batch;
+    }
+    ctx->t += 1;
+    ctx->next_layer = 0;
+    st = build_lists(ctx, forced, s);
+    ctx->last_stream = s;
+    return st;
+}
+
+namespace {
+
+asrkf_status sync_ctx(asrkf_ctx* ctx) {
+    HIP_OK(ctx, hipStreamSynchronize(ctx->last_stream));
+    HIP_OK(ctx, hipDeviceSynchronize());
+    return ASRKF_OK;
+}
+
+asrkf_status collect_timing(asrkf_ctx* ctx) {
+    for (auto& ev : ctx->ev_used) {
+        float ms = 0.f;
+        HIP_OK(ctx, hipEventElapsedTime(&ms, ev.first, ev.second));
+        ctx->attn_ms_done += ms;
+        ctx->attn_launches += 1;
+        ctx->ev_free.push_back(ev);
+    }
+    ctx->ev_used.clear();
+    return ASRKF_OK;
+}
+
+}  // namespace
+
+asrkf_status asrkf_stats(asrkf_ctx* ctx, asrkf_stats_t* out) {
+    asrkf_status st = check_ctx(ctx);
+    if (st != ASRKF_OK) return st;
+    if (!out) return fail(ASRKF_EINVAL, "null output");
+    st = sync_ctx(ctx);
+    if (st != ASRKF_OK) return st;
+    st = collect_timing(ctx);
+    if (st != ASRKF_OK) return st;
+    const asrkf_config& c = ctx->cfg;
+    const size_t inst = (size_t)c.n_layers * c.batch;
+    unsigned long long cnt[8];
+    std::vector<int32_t> na(inst);
+    HIP_OK(ctx, hipMemcpy(cnt, ctx->counters, sizeof cnt, hipMemcpyDeviceToHost));
+    HIP_OK(ctx, hipMemcpy(na.data(), ctx->n_active, inst * 4, hipMemcpyDeviceToHost));
+    memset(out, 0, sizeof *out);
+    out->step = ctx->t;
+    int64_t total = 0, active = 0, current = 0;
+    for (int b = 0; b < c.batch; ++b) total += (int64_t)(ctx->plen_host[b] + ctx->t) * c.n_layers;
+    if (ctx->lists_ready) {
+        for (size_t i = 0; i < inst; ++i) { current += na[i]; active += na[i] - 1; }
+    } else {
+        active = total;
+    }
+    out->total_positions = total;
+    out->active_positions = active;
+    out->attended_total = ctx->lists_ready ? (int64_t)cnt[0] - current : 0;
+    for (int i = 1; i < 4; ++i) out->recoveries[i] = (int64_t)cnt[i] + ctx->host_recoveries[i];
+    out->rr_requests = (int64_t)cnt[5];
+    out->attn_launches = ctx->attn_launches;
+    out->attn_kernel_ms = ctx->attn_ms_done;
+    out->compression = total > 0 ? 1.0 - (double)active / (double)total : 0.0;
+    return ASRKF_OK;
+}
+
+asrkf_status asrkf_stats_reset(asrkf_ctx* ctx) {
+    asrkf_status st = check_ctx(ctx);
+    if (st != ASRKF_OK) return st;
+    st = sync_ctx(ctx);
+    if (st != ASRKF_OK) return st;
+    st = collect_timing(ctx);
+    if (st != ASRKF_OK) return st;
+    const asrkf_config& c = ctx->cfg;
+    const size_t inst = (size_t)c.n_layers * c.batch;
+    std::vector<int32_t> na(inst);
+    HIP_OK(ctx, hipMemcpy(na.data(), ctx->n_active, inst * 4, hipMemcpyDeviceToHost));
+    // keep the lists of the coming step counted, drop everything before it
+    unsigned long long cnt[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+    if (ctx->lists_ready)
+        for (size_t i = 0; i < inst; ++i) cnt[0] += (unsigned long long)na[i];
+    HIP_OK(ctx, hipMemcpy(ctx->counters, cnt, sizeof cnt, hipMemcpyHostToDevice));
+    for (int i = 0; i < 4; ++i) ctx->host_recoveries[i] = 0;
+    ctx->attn_ms_done = 0.0;
+    ctx->attn_launches = 0;
+    return ASRKF_OK;
+}
+
+asrkf_status asrkf_set_timing(asrkf_ctx* ctx, int32_t enable) {
+    asrkf_status st = check_ctx(ctx);
+    if (st != ASRKF_OK) return st;
+    ctx->timing = enable != 0;
+    return ASRKF_OK;
+}
+
+asrkf_status asrkf_get_state(asrkf_ctx* ctx, int32_t layer, int32_t seq, int32_t* n_positions,
+                             int32_t* unfreeze_step, int32_t* count, uint8_t* frozen,
+                             int32_t* active, int32_t* n_active) {
+    asrkf_status st = check_ctx(ctx);
+    if (st != ASRKF_OK) return st;
+    const asrkf_config& c = ctx->cfg;
+    if (layer < 0 || layer >= c.n_layers || seq < 0 || seq >= c.batch)
+        return fail(ASRKF_EINVAL, "layer or sequence out of range");
+    st = sync_ctx(ctx);
+    if (st != ASRKF_OK) return st;
+    const int n = ctx->plen_host[seq] + ctx->t;
+    const size_t off = ((size_t)layer * c.batch + seq) * ctx->cap;
+    std::vector<int32_t> U(n > 0 ? n : 1);
+    if (n > 0) HIP_OK(ctx, hipMemcpy(U.data(), ctx->unfreeze + off, (size_t)n * 4, hipMemcpyDeviceToHost));
+    if (n_positions) *n_positions = n;
+    if (unfreeze_step && n > 0) memcpy(unfreeze_step, U.data(), (size_t)n * 4);
+    if (count && n > 0) HIP_OK(ctx, hipMemcpy(count, ctx->count + off, (size_t)n * 4, hipMemcpyDeviceToHost));
+    if (frozen)
+        for (int p = 0; p < n; ++p) frozen[p] = U[p] > ctx->t + 1 ? 1 : 0;
+    if (active || n_active) {
+        int32_t na = 0;
+        if (ctx->lists_ready) {
+            HIP_OK(ctx, hipMemcpy(&na, ctx->n_active + ((size_t)layer * c.batch + seq), 4,
+                                  hipMemcpyDeviceToHost));
+            if (active && na > 0)
+                HIP_OK(ctx, hipMemcpy(active, ctx->list + off, (size_t)na * 4, hipMemcpyDeviceToHost));
+        } else {
+            // before the first step every prompt position attends, then the new token
+            na = n + 1;
+            if (active) for (int p = 0; p <= n; ++p) active[p] = p;
+        }
+        if (n_active) *n_active = na;
+    }
+    return ASRKF_OK;
+}
+
+asrkf_status asrkf_get_seq(asrkf_ctx* ctx, int32_t seq, float* entropy, float* pmax,
+                           int32_t* escalation, int32_t* level) {
+    asrkf_status st = check_ctx(ctx);
+    if (st != ASRKF_OK) return st;
+    if (seq < 0 || seq >= ctx->cfg.batch) return fail(ASRKF_EINVAL, "sequence out of range");
+    st = sync_ctx(ctx);
+    if (st != ASRKF_OK) return st;
+    if (entropy) HIP_OK(ctx, hipMemcpy(entropy, ctx->entropy + seq, 4, hipMemcpyDeviceToHost));
+    if (pmax) HIP_OK(ctx, hipMemcpy(pmax, ctx->pmax + seq, 4, hipMemcpyDeviceToHost));
+    if (escalation) HIP_OK(ctx, hipMemcpy(escalation, ctx->escalation + seq, 4, hipMemcpyDeviceToHost));
+    if (level) HIP_OK(ctx, hipMemcpy(level, ctx->level + seq, 4, hipMemcpyDeviceToHost));
+    return ASRKF_OK;
+}
+
+void asrkf_destroy(asrkf_ctx* ctx) {
+    if (!ctx) return;
+    (void)hipDeviceSynchronize();
+    free_all(ctx);
+    delete ctx;
+}
+
+}  // extern "C"

@@ -1,0 +1,231 @@
+"""Drive the GPU library and the CPU oracle over the same seeded inputs.
+
+Inputs come only from ``synth`` (host generator); expected values only from
+``oracle``.  The GPU side goes through the C ABI (ctypes binding).
+"""
+from __future__ import annotations
+
+import numpy as np
+
+import oracle
+from synth import gen
+
+# acceptance bounds for attention outputs computed from bf16/fp32 K/V
+ATOL = 2e-2
+RTOL_NORM = 1e-2
+ENTROPY_TOL = 1e-3
+MARGIN = 1e-3
+
+
+# --------------------------------------------------------------------------
+# inputs
+# --------------------------------------------------------------------------
+
+class Inputs:
+    """Host copies of a workload's inputs, generated on demand and cached."""
+
+    def __init__(self, w, attempts=None):
+        self.w = w
+        self.attempts = attempts or {}
+        self._kv = {}
+
+    def kv(self, layer, seq):
+        key = (layer, seq)
+        if key not in self._kv:
+            n = self.w.prefill[seq] + self.w.steps
+            self._kv[key] = gen.kv_rows(self.w, layer, seq, 0, n, self.attempts.get(key))
+        return self._kv[key]
+
+    def prompt(self, layer, seq):
+        K, V = self.kv(layer, seq)
+        P = self.w.prefill[seq]
+        return K[:P], V[:P]
+
+    def new_token(self, layer, seq, t):
+        K, V = self.kv(layer, seq)
+        p = self.w.prefill[seq] + t - 1
+        return K[p], V[p]
+
+    def q(self, layer, seq, t):
+        return gen.q_row(self.w, layer, seq, t)
+
+    def logits(self, seq, t):
+        return gen.logits_row(self.w, seq, t)
+
+
+def fix_margin(w, max_rounds=20):
+    """Re-draw keys until every relevance score keeps |s - tau| >= MARGIN at
+    every step (tiny workloads; scores from the oracle over all positions)."""
+    attempts = {}
+    for _ in range(max_rounds):
+        inp = Inputs(w, attempts)
+        bad_any = False
+        for l in range(w.n_layers):
+            for b in range(w.batch):
+                K, _ = inp.kv(l, b)
+                P = w.prefill[b]
+                bad = np.zeros(len(K), bool)
+                for t in range(1, w.steps + 1):
+                    n = P + t
+                    s = oracle.relevance(inp.q(l, b, t), K[:n])
+                    bad[:n] |= np.abs(s - w.tau) < MARGIN
+                if bad.any():
+                    bad_any = True
+                    a = attempts.setdefault((l, b), np.zeros(len(K), np.int64))
+                    a[bad] += 1
+        if not bad_any:
+            return attempts
+    raise RuntimeError("margin not reached")
+
+
+def score_quantile(w, qtl, layer=0, seq=0):
+    inp = Inputs(w)
+    K, _ = inp.kv(layer, seq)
+    P = w.prefill[seq]
+    s = np.concatenate([oracle.relevance(inp.q(layer, seq, t), K[: P + t])
+                        for t in range(1, w.steps + 1)])
+    return float(np.quantile(s, qtl))
+
+
+# --------------------------------------------------------------------------
+# oracle side
+# --------------------------------------------------------------------------
+
+def oracle_levels(w, inp, seq, modes=None, with_logits=True):
+    """Recovery level applied after each step of one sequence."""
+    if modes is None and with_logits:
+        ent = [oracle.entropy(inp.logits(seq, t)) for t in range(1, w.steps + 1)]
+        levels, rr = oracle.recovery_schedule(ent, w.entropy_spike, w.conf_drop)
+        return levels, ent
+    levels = []
+    for t in range(1, w.steps + 1):
+        m = 0 if modes is None else modes.get(t, 0)
+        levels.append(m if m in (1, 2, 3) else 0)
+    ent = ([oracle.entropy(inp.logits(seq, t)) for t in range(1, w.steps + 1)]
+           if with_logits else None)
+    return levels, ent
+
+
+def run_oracle(w, inp, instances, modes=None, with_logits=True, steps=None, record=None):
+    """Per instance: list over steps of dict(out, frozen, timer, count, active_next)."""
+    steps = w.steps if steps is None else steps
+    res = {}
+    for (l, b) in instances:
+        levels, _ = oracle_levels(w, inp, b, modes, with_logits)
+        K, V = inp.prompt(l, b)
+        inst = oracle.Instance(K, V, w.window_K, w.tau, w.k_soft,
+                               capacity=w.prefill[b] + steps + 1)
+        recs = []
+        for t in range(1, steps + 1):
+            kn, vn = inp.new_token(l, b, t)
+            rec = inst.step(inp.q(l, b, t), kn, vn)
+            if levels[t - 1]:
+                inst.recover(levels[t - 1], w.wr_last_N)
+            if record is None or record(t):
+                timer, count, frozen = inst.state()
+                act = np.concatenate([np.nonzero(~frozen)[0], [inst.n]])
+                recs.append(dict(t=t, out=rec.out, frozen=frozen, timer=timer, count=count,
+                                 active_next=act, scores=rec.scores, attended=rec.active))
+        res[(l, b)] = recs
+    return res
+
+
+# --------------------------------------------------------------------------
+# GPU side
+# --------------------------------------------------------------------------
+
+def _dev(x, dtype):
+    import torch
+    t = torch.from_numpy(np.ascontiguousarray(x, dtype=np.float32))
+    if dtype == "bf16":
+        t = t.to(torch.bfloat16)           # exact: values are bf16-representable
+    return t.cuda()
+
+
+def run_gpu(w, inp, instances, modes=None, with_logits=True, steps=None, record=None,
+            timing=False):
+    """Run the library; per instance a list of dict(out, unfreeze, count, frozen,
+    active_next) for the recorded steps; per sequence the entropy monitor."""
+    import torch
+    import paper_2512_11221_amd as A
+
+    steps = w.steps if steps is None else steps
+    cfg = A.make_config(w.n_layers, w.batch, w.n_q_heads, w.n_kv_heads, w.head_dim,
+                        w.max_ctx, w.window_K, w.tau, w.k_soft, w.vocab,
+                        entropy_spike=w.entropy_spike, conf_drop=w.conf_drop,
+                        wr_last_N=w.wr_last_N, dtype=w.dtype)
+    ctx = A.asrkf_init(cfg)
+    res = {key: [] for key in instances}
+    seqmon = {b: [] for b in range(w.batch)}
+    stats = []
+    try:
+        for l in range(w.n_layers):
+            for b in range(w.batch):
+                K, V = inp.prompt(l, b)
+                if len(K):
+                    A.asrkf_prefill(ctx, l, b, _dev(K, w.dtype), _dev(V, w.dtype), len(K))
+        torch.cuda.synchronize()
+        for t in range(1, steps + 1):
+            outs = []
+            keep = []
+            for l in range(w.n_layers):
+                q = np.stack([inp.q(l, b, t) for b in range(w.batch)])
+                kn = np.stack([inp.new_token(l, b, t)[0] for b in range(w.batch)])
+                vn = np.stack([inp.new_token(l, b, t)[1] for b in range(w.batch)])
+                dq, dk, dv = _dev(q, w.dtype), _dev(kn, w.dtype), _dev(vn, w.dtype)
+                out = torch.empty((w.batch, w.n_q_heads, w.head_dim), dtype=torch.float32,
+                                  device="cuda")
+                A.asrkf_decode_step(ctx, l, dq, dk, dv, out)
+                keep += [dq, dk, dv]
+                outs.append(out)
+            mode = A.AUTO if modes is None else modes.get(t, A.NONE)
+            if with_logits:
+                lg = _dev(np.stack([inp.logits(b, t) for b in range(w.batch)]), "f32")
+                keep.append(lg)
+                A.asrkf_restore(ctx, lg, mode)
+            else:
+                A.asrkf_restore(ctx, None, mode)
+            torch.cuda.synchronize()
+            if record is None or record(t):
+                for (l, b) in instances:
+                    st = A.asrkf_get_state(ctx, l, b, w.max_ctx)
+                    st["out"] = outs[l][b].cpu().numpy()
+                    st["t"] = t
+                    res[(l, b)].append(st)
+                for b in range(w.batch):
+                    seqmon[b].append(A.asrkf_get_seq(ctx, b))
+                stats.append(A.asrkf_stats(ctx))
+            del keep
+    finally:
+        A.asrkf_destroy(ctx)
+    return res, seqmon, stats
+
+
+# --------------------------------------------------------------------------
+# comparison
+# --------------------------------------------------------------------------
+
+def compare_instance(gpu_recs, ora_recs, check_out=True):
+    """Bit-exact states; attention outputs within the acceptance bound.
+    Returns the largest absolute output error seen."""
+    worst = 0.0
+    assert len(gpu_recs) == len(ora_recs)
+    for g, o in zip(gpu_recs, ora_recs):
+        t = o["t"]
+        assert g["t"] == t
+        n = len(o["frozen"])
+        assert g["n"] == n, (t, g["n"], n)
+        np.testing.assert_array_equal(g["frozen"], o["frozen"], err_msg=f"frozen mask, step {t}")
+        np.testing.assert_array_equal(g["count"], o["count"], err_msg=f"counts, step {t}")
+        fz = o["frozen"]
+        np.testing.assert_array_equal(g["unfreeze"][fz] - (t + 1), o["timer"][fz],
+                                      err_msg=f"remaining timers, step {t}")
+        np.testing.assert_array_equal(g["active"], o["active_next"], err_msg=f"active list, step {t}")
+        if check_out:
+            ref = o["out"]
+            err = np.abs(g["out"].astype(np.float64) - ref)
+            worst = max(worst, float(err.max()))
+            assert err.max() <= ATOL, (t, float(err.max()))
+            rel = np.linalg.norm(g["out"] - ref) / max(np.linalg.norm(ref), 1e-30)
+            assert rel <= RTOL_NORM, (t, rel)
+    return worst

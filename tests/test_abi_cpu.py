@@ -1,0 +1,65 @@
+"""Host-side checks of the C ABI (no GPU needed): exported symbols, the exact
+Eq. 3 table against the oracle, and argument validation."""
+import math
+import re
+import os
+
+import numpy as np
+import pytest
+
+import oracle
+import paper_2512_11221_amd as A
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def _declared():
+    with open(os.path.join(ROOT, "include", "asrkf.h")) as f:
+        text = f.read()
+    return sorted(set(re.findall(r"\b(asrkf_[a-z_]+)\s*\(", text)))
+
+
+def test_every_declared_symbol_is_exported():
+    lib = A.load()
+    names = _declared()
+    assert {"asrkf_init", "asrkf_decode_step", "asrkf_restore", "asrkf_stats"} <= set(names)
+    for name in names:
+        assert hasattr(lib, name), name
+
+
+@pytest.mark.parametrize("k", [2.0, 1.5, 0.75, 3.0, 1.0, 2.5, 0.3, 7.25])
+def test_schedule_table_matches_oracle(k):
+    tab = A.asrkf_schedule_table(k, 3000)
+    ref = oracle.duration_table(2999, k)
+    np.testing.assert_array_equal(tab, ref)
+
+
+def test_schedule_table_rejects_bad_k():
+    for k in (0.0, -1.0, math.inf, math.nan, 1e-5, 1e6):
+        with pytest.raises(A.AsrkfError):
+            A.asrkf_schedule_table(k, 10)
+
+
+BASE = dict(n_layers=1, batch=1, n_q_heads=8, n_kv_heads=2, head_dim=64, max_ctx=600,
+            window_K=32, tau=0.5, k_soft=2.0, vocab=1024)
+
+
+@pytest.mark.parametrize("bad", [
+    dict(head_dim=96), dict(n_kv_heads=3), dict(n_q_heads=24, n_kv_heads=2),
+    dict(n_kv_heads=16, n_q_heads=16), dict(batch=0), dict(batch=5000), dict(n_layers=0),
+    dict(max_ctx=1), dict(window_K=-1), dict(k_soft=0.0), dict(tau=math.nan), dict(vocab=0),
+    dict(spill_min_D=2),
+])
+def test_init_rejects_invalid_config(bad):
+    cfg = A.make_config(**{**BASE, **bad})
+    with pytest.raises(A.AsrkfError) as e:
+        A.asrkf_init(cfg)
+    assert e.value.code == A._lib.EINVAL
+
+
+def test_null_context_is_einval():
+    lib = A.load()
+    assert lib.asrkf_set_timing(None, 1) == A._lib.EINVAL
+    assert lib.asrkf_restore(None, None, 0, None) == A._lib.EINVAL
+    assert "null context" in A.asrkf_last_error()
+    lib.asrkf_destroy(None)

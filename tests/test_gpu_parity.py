@@ -1,0 +1,148 @@
+"""GPU parity: the HIP path (through the C ABI) against the CPU oracle.
+
+Freeze masks, counts, remaining timers and active lists are compared bit for
+bit; attention outputs within 2e-2 max-abs and 1e-2 relative (norm); entropy
+within 1e-3 nats.  Inputs come from the seeded generator; every relevance
+score stays at least 1e-3 away from tau (by construction for the heavy-hitter
+recipe, by re-drawing keys for the Gaussian recipe).
+"""
+import math
+
+import numpy as np
+import pytest
+
+from synth import gen
+from tests import _harness as H
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def gpu():
+    torch = pytest.importorskip("torch")
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    import paper_2512_11221_amd as A
+    A.load()          # raises when the library is not built: no fallback
+    return torch
+
+
+def _all_instances(w):
+    return [(l, b) for l in range(w.n_layers) for b in range(w.batch)]
+
+
+def _parity(w, inp, modes=None, with_logits=True, instances=None, record=None, check_out=True):
+    instances = instances or _all_instances(w)
+    g, mon, stats = H.run_gpu(w, inp, instances, modes, with_logits, record=record)
+    o = H.run_oracle(w, inp, instances, modes, with_logits, record=record)
+    worst = 0.0
+    for key in instances:
+        worst = max(worst, H.compare_instance(g[key], o[key], check_out))
+    print(f"{w.name}: worst |out - oracle| = {worst:.3e}")
+    return g, o, mon, stats
+
+
+def _tiny_freezing(**kw):
+    w0 = gen.tiny()
+    tau = H.score_quantile(w0, 0.6)
+    w = gen.tiny(tau=tau, **kw)
+    return w, H.Inputs(w, H.fix_margin(w))
+
+
+def test_tiny_freezing_nothing_is_dense():
+    w = gen.tiny()                          # scores ~6.4 >> tau = 0.5
+    inp = H.Inputs(w)
+    g, o, _, _ = _parity(w, inp)
+    for r in o[(0, 0)]:
+        assert not r["frozen"].any()
+    for r in g[(0, 0)]:
+        assert len(r["active"]) == r["n"] + 1
+
+
+def test_tiny_with_freezing():
+    w, inp = _tiny_freezing()
+    g, o, _, _ = _parity(w, inp)
+    frac = np.mean([r["frozen"].mean() for r in o[(0, 0)]])
+    assert 0.05 < frac < 0.9, frac           # the run does freeze and restore
+
+
+def test_tiny_entropy_driven_recovery():
+    flat = (40, 50, 51, 60, 61, 62)
+    w, inp = _tiny_freezing(entropy_spike=6.5, flat_logit_steps=flat)
+    # every step's entropy stays 1e-2 away from theta_H; spikes only where planted
+    ent = [H.oracle.entropy(inp.logits(0, t))[0] for t in range(1, w.steps + 1)]
+    assert min(abs(e - 6.5) for e in ent) >= 1e-2
+    assert [t for t, e in enumerate(ent, 1) if e > 6.5] == list(flat)
+    g, o, mon, stats = _parity(w, inp)
+    levels, _ = H.oracle_levels(w, inp, 0)
+    assert [m["level"] for m in mon[0]] == levels
+    assert max(levels) == 3
+    for m, e in zip(mon[0], ent):
+        assert abs(m["entropy"] - e) <= H.ENTROPY_TOL
+    assert stats[-1]["recoveries"][1:] == [3, 2, 1]
+
+
+@pytest.mark.parametrize("with_logits", [False, True])
+def test_forced_recovery_modes(with_logits):
+    import paper_2512_11221_amd as A
+    w, inp = _tiny_freezing()
+    modes = {20: A.SR, 33: A.WR, 47: A.FR, 55: A.SR}
+    _parity(w, inp, modes=modes, with_logits=with_logits)
+
+
+def test_llama8b_one_layer_full_run():
+    w = gen.llama8b_1layer()
+    inp = H.Inputs(w)
+    g, o, mon, stats = _parity(w, inp)
+    ent = [H.oracle.entropy(inp.logits(0, t))[0] for t in range(1, w.steps + 1)]
+    for m, e in zip(mon[0], ent):
+        assert abs(m["entropy"] - e) <= H.ENTROPY_TOL
+    # heavy-hitter recipe: active fraction between the hitter share and 1
+    last = o[(0, 0)][-1]
+    assert 0.3 < 1 - last["frozen"].mean() <= 1.0
+
+
+@pytest.mark.parametrize("tau", [-1.0, math.inf])
+def test_bf16_gaussian_multilayer_ragged(tau):
+    """Strong logits (q, k ~ N(0,1) at D = 128), two layers, three sequences of
+    very different prompt lengths; tau below every score (dense) or above
+    every score (every out-of-window token flagged each step)."""
+    w = gen.Workload(name="bf16-gauss", seed=gen.SEED + 21, n_layers=2, batch=3, n_q_heads=32,
+                     n_kv_heads=8, head_dim=128, dtype="bf16", prefill=[700, 1, 300], steps=40,
+                     window_K=16, tau=tau, k_soft=2.0, vocab=1000, logit_sigma=2.0,
+                     recipe="gauss")
+    _parity(w, H.Inputs(w))
+
+
+@pytest.mark.parametrize("shape", [
+    dict(n_q_heads=8, n_kv_heads=8, head_dim=128, dtype="bf16"),    # G = 1
+    dict(n_q_heads=16, n_kv_heads=2, head_dim=128, dtype="bf16"),   # G = 8
+    dict(n_q_heads=8, n_kv_heads=4, head_dim=64, dtype="bf16"),     # G = 2, D = 64
+    dict(n_q_heads=8, n_kv_heads=2, head_dim=128, dtype="f32"),     # fp32, D = 128
+])
+def test_shapes_flag_all(shape):
+    w = gen.Workload(name="shape", seed=gen.SEED + 31, n_layers=1, batch=2, prefill=[190, 77],
+                     steps=70, window_K=0, tau=math.inf, k_soft=0.75, vocab=64,
+                     logit_sigma=1.0, recipe="gauss", **shape)
+    _parity(w, H.Inputs(w))
+
+
+def test_ragged_heavy_hitters_multilayer():
+    w = gen.Workload(name="hh-ragged", seed=gen.SEED + 41, n_layers=2, batch=6, n_q_heads=32,
+                     n_kv_heads=8, head_dim=128, dtype="bf16",
+                     prefill=[1, 17, 64, 333, 1000, 2049], steps=48, window_K=32, tau=0.5,
+                     k_soft=2.0, vocab=128256, logit_sigma=3.0, recipe="hh",
+                     f_hh=[0.2, 0.3, 0.5, 0.35, 0.25, 0.45])
+    s_cold, s_hot = gen.hh_relevance_bounds(w)
+    assert s_cold < w.tau - H.MARGIN and s_hot > w.tau + H.MARGIN
+    _parity(w, H.Inputs(w))
+
+
+def test_bitwise_determinism():
+    w, inp = _tiny_freezing()
+    a, _, _ = H.run_gpu(w, inp, [(0, 0)])
+    b, _, _ = H.run_gpu(w, inp, [(0, 0)])
+    for x, y in zip(a[(0, 0)], b[(0, 0)]):
+        np.testing.assert_array_equal(x["out"], y["out"])
+        np.testing.assert_array_equal(x["unfreeze"], y["unfreeze"])
+        np.testing.assert_array_equal(x["active"], y["active"])
