@@ -1,5 +1,5 @@
 // Active-set GQA flash-decode for gfx950, fused with the relevance score and
-// the freeze schedule.
+// the freeze schedule, and the per-layer split combine.
 //
 // Per launch (one layer, every sequence):
 //   Eq. 1  o_h = softmax_j(q_h . k_j / sqrt(D)) v_j over the active list A_t;
@@ -8,40 +8,47 @@
 //          when d = floor(sqrt(c_j)/k) >= 1, the unfreeze step U_j = t + d.
 //
 // Work decomposition.  The active lists of all sequences, concatenated, are
-// cut into equal contiguous ranges, one per workgroup of a persistent grid;
-// each workgroup derives the cut from the active counts on the device and
-// leaves one partial (m, l, acc) per sequence its range touches, at slot
-// (workgroup + sequence).  A workgroup has one wave per KV head; all its waves
-// walk the same tokens, so the per-token relevance is summed over every head
-// in LDS and the schedule applied in place.
+// cut into equal contiguous token ranges, one per workgroup of a fixed grid,
+// computed on the device from the active counts.  Inside a workgroup the
+// range is walked in tiles dealt round-robin to its waves (a static deal, so
+// every run sums in the same order).  The waves' softmax states are merged
+// through LDS once per sequence the range touches, giving one partial
+// (m, l, acc) of every query head at slot (workgroup + sequence).
 //
-// Lane layout inside a wave: 8 token slots x 8 lanes.  The 8 lanes of a slot
-// read one token's row of this KV head (D * elem bytes) as 16-byte pieces, so
-// each load instruction moves 8 contiguous 128-byte segments.  The row is
-// used by the G query heads of the group from registers (GQA sharing).  The
-// dot products are reduced across the 8 lanes with DPP; each slot keeps its
-// own running maximum so the inner loop has no cross-slot traffic; slots are
-// merged once per sequence segment.
+// Lane layout inside a wave: 8 slots x 8 lanes.  Slot s holds KV head
+// s % Hkv of token s / Hkv of the iteration (8 / Hkv tokens per iteration),
+// so a wave reads whole token rows (every KV head) and every load
+// instruction moves 8 contiguous 128-byte segments.  A slot's row serves the
+// G query heads of its KV head from registers (GQA sharing); dot products are
+// reduced over the slot's 8 lanes with DPP, the relevance over the token's
+// KV-head slots with lane exchanges, so the freeze decision is made in the
+// wave and applied by the workgroup after each chunk.
 #include "kernels.h"
 
 namespace asrkf {
 namespace {
 
-constexpr int kSlots = 8;      // tokens per wave per iteration
-constexpr int kUnroll = 4;     // iterations per tile
-constexpr int kMinPerGroup = 128;  // fewest tokens worth a workgroup
+constexpr int kWaves = 8;           // waves per workgroup
+constexpr int kUnroll = 4;          // iterations per tile
+constexpr int kChunk = 2048;        // tokens per LDS chunk (positions, freeze flags)
+constexpr int kMinPerGroup = 64;    // fewest tokens worth a workgroup
+constexpr int kDurCache = 512;      // Eq. 3 durations cached in LDS
+// raw buffer descriptor word 3 for gfx9-class targets (32-bit data, no swizzle)
+constexpr int kBufferFlags = 0x00020000;
+
+// A value the whole wave agrees on, moved to a scalar register.
+__device__ __forceinline__ int wave_uniform(int x) { return __builtin_amdgcn_readfirstlane(x); }
 
 template <int CTRL>
 __device__ __forceinline__ float dpp_mov(float v) {
     return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), CTRL, 0xF, 0xF, false));
 }
 
-// Sum over the 8 lanes of a slot; every lane of the slot gets the same bits.
-__device__ __forceinline__ float slot_sum(float v) {
-    v += dpp_mov<0xB1>(v);   // quad_perm [1,0,3,2]
-    v += dpp_mov<0x4E>(v);   // quad_perm [2,3,0,1]
-    v += dpp_mov<0x141>(v);  // row_half_mirror
-    return v;
+// value of lane (lane ^ mask) for mask in {8, 16, 32}
+template <int MASK>
+__device__ __forceinline__ float lane_xor(float v) {
+    if constexpr (MASK == 8) return dpp_mov<0x128>(v);    // row_ror:8
+    else return __shfl_xor(v, MASK);
 }
 
 __device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
@@ -108,14 +115,6 @@ __device__ __forceinline__ void lane_axpy(LaneAcc<BF16, D>& acc, float p, const 
     }
 }
 
-// Element index (within the D of a row) of lane element e for dim-lane r.
-template <bool BF16, int D>
-__device__ __forceinline__ int lane_dim(int r, int e) {
-    using R = Row<BF16, D>;
-    const int c = e / R::kPerChunk, i = e % R::kPerChunk;
-    return c * (128 / R::kElem) + r * R::kPerChunk + i;
-}
-
 // Token offsets of every sequence in the concatenated active lists:
 // seq_off[b] = sum of n_active[b'] for b' < b, seq_off[B] = T.  Wave 0 scans.
 __device__ void plan_ranges(const int32_t* n_active, int B, int32_t* seq_off) {
@@ -138,85 +137,108 @@ __device__ void plan_ranges(const int32_t* n_active, int B, int32_t* seq_off) {
         }
         if (tid == 63) seq_off[B] = incl;
     }
-    __syncthreads();
 }
 
-// Workgroups that share the work: enough that each gets kMinPerGroup tokens.
+// Workgroups that share the tokens: enough that each gets kMinPerGroup of them.
 __device__ __forceinline__ int active_groups(int T, int grid) {
     return max(1, min(grid, (T + kMinPerGroup - 1) / kMinPerGroup));
 }
 
-// Workgroup holding token x of the concatenated lists when T tokens are cut
-// into G ranges [floor(w T / G), floor((w+1) T / G)).
+// Workgroup holding token x when T tokens are cut into G ranges
+// [floor(w T / G), floor((w+1) T / G)).
 __device__ __forceinline__ int group_of(int64_t x, int64_t T, int64_t G) {
     return (int)(((x + 1) * G - 1) / T);
 }
 
+// Online-softmax state of one lane: its slot's G query heads.
 template <bool BF16, int D, int G>
-__global__ void __launch_bounds__(512)
+struct SoftState {
+    float m[G], l[G];
+    float acc[G][Row<BF16, D>::kPerLane];
+};
+
+// Fold state b into state a (both of the same lane), fixed order.
+template <bool BF16, int D, int G>
+__device__ __forceinline__ void fold(SoftState<BF16, D, G>& a, const float* bm, const float* bl,
+                                     const float (*bacc)[Row<BF16, D>::kPerLane]) {
+#pragma unroll
+    for (int h = 0; h < G; ++h) {
+        const float M = fmaxf(a.m[h], bm[h]);
+        const float sa = (a.m[h] == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(a.m[h] - M);
+        const float sb = (bm[h] == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(bm[h] - M);
+        a.l[h] = a.l[h] * sa + bl[h] * sb;
+#pragma unroll
+        for (int e = 0; e < Row<BF16, D>::kPerLane; ++e) a.acc[h][e] = a.acc[h][e] * sa + bacc[h][e] * sb;
+        a.m[h] = M;
+    }
+}
+
+template <bool BF16, int D, int G, int HKV>
+__global__ void __launch_bounds__(64 * kWaves)
 attention_kernel(AttnArgs a) {
     using R = Row<BF16, D>;
+    using S = SoftState<BF16, D, G>;
     constexpr int NC = R::kChunks;
     constexpr int EL = R::kPerLane;
+    constexpr int TPI = 8 / HKV;                 // tokens per iteration
+    constexpr int TT = kUnroll * TPI;            // tokens per tile
+    constexpr int NV = 2 * G + G * EL;           // floats of a lane's state
 
     extern __shared__ int32_t lds[];
-    int32_t* seq_off = lds;                           // [B + 1]
-    int32_t* pos_lds = lds + ((a.B + 1 + 3) & ~3);    // [kChunkMax]
-    float* rel_lds = reinterpret_cast<float*>(pos_lds + kChunkMax);  // [Hkv][kChunkMax]
+    int32_t* seq_off = lds;                                      // [B + 1]
+    int32_t* dur_lds = lds + ((a.B + 1 + 3) & ~3);               // [kDurCache]
+    int32_t* pos_lds = dur_lds + kDurCache;                      // [kChunk]
+    uint8_t* flag_lds = reinterpret_cast<uint8_t*>(pos_lds + kChunk);   // [kChunk]
+    float* merge_lds = reinterpret_cast<float*>(flag_lds + kChunk);    // [kWaves/2][NV][64]
 
+    for (int i = threadIdx.x; i < kDurCache; i += blockDim.x) dur_lds[i] = a.dur[min(i, a.dur_len - 1)];
     plan_ranges(a.n_active, a.B, seq_off);
-    const int T = seq_off[a.B];
+    __syncthreads();
+    const int T = wave_uniform(seq_off[a.B]);
     const int Gn = active_groups(T, gridDim.x);
     if (blockIdx.x == 0) {
         for (int b = threadIdx.x; b < a.B; b += blockDim.x) {
-            const int s0 = seq_off[b], s1 = seq_off[b + 1];
-            a.slot_first[b] = s1 > s0 ? group_of(s0, T, Gn) + b : 0;
-            a.slot_end[b] = s1 > s0 ? group_of(s1 - 1, T, Gn) + b + 1 : 0;
+            const int x0 = seq_off[b], x1 = seq_off[b + 1];
+            a.slot_first[b] = x1 > x0 ? group_of(x0, T, Gn) + b : 0;
+            a.slot_end[b] = x1 > x0 ? group_of(x1 - 1, T, Gn) + b + 1 : 0;
         }
     }
     const int w = blockIdx.x;
     if (w >= Gn) return;
 
+    const int wave = wave_uniform(threadIdx.x >> 6);
     const int lane = threadIdx.x & 63;
-    const int g = threadIdx.x >> 6;          // KV head of this wave
     const int slot = lane >> 3;
+    const int tk = slot / HKV;                    // token of the iteration
+    const int g = slot % HKV;                     // KV head
     const int r = lane & 7;
-    const size_t row_stride = (size_t)a.Hkv * R::kBytes;   // bytes per token (all KV heads)
+    const int row_stride = HKV * R::kBytes;       // bytes per token (all KV heads)
+    const int lane_off = g * R::kBytes + r * 16;
 
-    int lo = (int)((int64_t)w * T / Gn);
-    const int hi = (int)((int64_t)(w + 1) * T / Gn);
+    int x = wave_uniform((int)((int64_t)w * T / Gn));
+    const int x_end = wave_uniform((int)((int64_t)(w + 1) * T / Gn));
     int b = 0;
     {
-        int l0 = 0, h0 = a.B - 1;             // last b with seq_off[b] <= lo
+        int l0 = 0, h0 = a.B - 1;                 // last b with seq_off[b] <= x
         while (l0 < h0) {
             const int mid = (l0 + h0 + 1) >> 1;
-            if (seq_off[mid] <= lo) l0 = mid; else h0 = mid - 1;
+            if (wave_uniform(seq_off[mid]) <= x) l0 = mid; else h0 = mid - 1;
         }
         b = l0;
     }
-
-    while (lo < hi) {
-        while (seq_off[b + 1] <= lo) ++b;     // skip sequences with nothing listed
-        const int nb = seq_off[b + 1] - seq_off[b];
-        const int i0 = lo - seq_off[b];
-        const int i1 = min(hi, seq_off[b + 1]) - seq_off[b];
+    while (x < x_end) {
+        while (wave_uniform(seq_off[b + 1]) <= x) ++b;   // skip empty lists
+        const int sb = wave_uniform(seq_off[b]);
+        const int se = wave_uniform(seq_off[b + 1]);
+        const int nb = se - sb;
+        const int i0 = x - sb;
+        const int i1 = min(se, x_end) - sb;
         const int n_pos = a.plen[b] + a.t;       // positions after the append
-        const int new_pos = n_pos - 1;
-        const int32_t* list_b = a.list + (size_t)b * a.cap;
+        const int wedge = n_pos - a.window_K;    // positions < wedge are outside the window
+        const size_t seq_row = (size_t)b * a.cap;
+        const size_t seg = seq_row * row_stride;
+        const int32_t* list_b = a.list + seq_row;
 
-        // append: the workgroup holding the new position copies it into the cache
-        if (i1 == nb) {
-            const size_t dst = ((size_t)b * a.cap + new_pos) * row_stride;
-            const size_t src = (size_t)b * row_stride;
-            for (size_t o = threadIdx.x * 16; o < row_stride; o += blockDim.x * 16) {
-                *reinterpret_cast<uint4*>((char*)a.kpool_w + dst + o) =
-                    *reinterpret_cast<const uint4*>((const char*)a.knew + src + o);
-                *reinterpret_cast<uint4*>((char*)a.vpool_w + dst + o) =
-                    *reinterpret_cast<const uint4*>((const char*)a.vnew + src + o);
-            }
-        }
-
-        // query heads g*G .. g*G+G-1, this lane's elements
         uint4 qr[G][NC];
         {
             const char* qb = (const char*)a.q + ((size_t)b * a.Hq + (size_t)g * G) * R::kBytes;
@@ -226,204 +248,316 @@ attention_kernel(AttnArgs a) {
                 for (int c = 0; c < NC; ++c)
                     qr[h][c] = *reinterpret_cast<const uint4*>(qb + h * R::kBytes + c * 128 + r * 16);
         }
-
-        float m[G], l[G], acc[G][EL];
+        S st;
 #pragma unroll
         for (int h = 0; h < G; ++h) {
-            m[h] = -INFINITY;
-            l[h] = 0.f;
+            st.m[h] = -INFINITY;
+            st.l[h] = 0.f;
 #pragma unroll
-            for (int e = 0; e < EL; ++e) acc[h][e] = 0.f;
+            for (int e = 0; e < EL; ++e) st.acc[h][e] = 0.f;
         }
+        const int nbytes = a.cap * row_stride;
+        const __amdgpu_buffer_rsrc_t rk = __builtin_amdgcn_make_buffer_rsrc(
+            (void*)((const char*)a.kpool + seg), (short)0, nbytes, kBufferFlags);
+        const __amdgpu_buffer_rsrc_t rv = __builtin_amdgcn_make_buffer_rsrc(
+            (void*)((const char*)a.vpool + seg), (short)0, nbytes, kBufferFlags);
 
-        const char* kbase = (const char*)a.kpool + (size_t)b * a.cap * row_stride + g * R::kBytes;
-        const char* vbase = (const char*)a.vpool + (size_t)b * a.cap * row_stride + g * R::kBytes;
-        const char* knew_row = (const char*)a.knew + ((size_t)b * a.Hkv + g) * R::kBytes;
-        const char* vnew_row = (const char*)a.vnew + ((size_t)b * a.Hkv + g) * R::kBytes;
-        const int wedge = n_pos - a.window_K;    // positions < wedge are outside the window
-
-        for (int c0 = i0; c0 < i1; c0 += kChunkMax) {
-            const int len = min(kChunkMax, i1 - c0);
-            for (int i = threadIdx.x; i < len; i += blockDim.x) pos_lds[i] = list_b[c0 + i];
+        for (int c0 = i0; c0 < i1; c0 += kChunk) {
+            const int len = min(kChunk, i1 - c0);
+            if (c0 + len == nb) {
+                // this chunk ends with the new token: append its row to the cache first
+                const size_t dst = seg + (size_t)(n_pos - 1) * row_stride;
+                const size_t src = (size_t)b * row_stride;
+                for (int o = threadIdx.x * 16; o < row_stride; o += blockDim.x * 16) {
+                    *reinterpret_cast<uint4*>((char*)a.kpool_w + dst + o) =
+                        *reinterpret_cast<const uint4*>((const char*)a.knew + src + o);
+                    *reinterpret_cast<uint4*>((char*)a.vpool_w + dst + o) =
+                        *reinterpret_cast<const uint4*>((const char*)a.vnew + src + o);
+                }
+            }
+            for (int i = threadIdx.x; i < len; i += blockDim.x) {
+                pos_lds[i] = list_b[c0 + i];
+                flag_lds[i] = 0;
+            }
+            __threadfence_block();
             __syncthreads();
 
-            for (int base = 0; base < len; base += kSlots * kUnroll) {
+            for (int tb = wave * TT; tb < len; tb += kWaves * TT) {
                 uint4 kr[kUnroll][NC], vr[kUnroll][NC];
                 bool valid[kUnroll];
+                int pos[kUnroll];
 #pragma unroll
                 for (int u = 0; u < kUnroll; ++u) {
-                    const int idx = base + u * kSlots + slot;
+                    const int idx = tb + u * TPI + tk;
                     valid[u] = idx < len;
-                    const int p = pos_lds[valid[u] ? idx : 0];
-                    const char* kp = (p == new_pos) ? knew_row : kbase + (size_t)p * row_stride;
-                    const char* vp = (p == new_pos) ? vnew_row : vbase + (size_t)p * row_stride;
+                    pos[u] = pos_lds[valid[u] ? idx : tb];
+                    int vo = lane_off, so = 0;
+                    if constexpr (TPI == 1) so = wave_uniform(pos[u]) * row_stride;
+                    else vo += pos[u] * row_stride;
 #pragma unroll
                     for (int c = 0; c < NC; ++c) {
-                        kr[u][c] = *reinterpret_cast<const uint4*>(kp + c * 128 + r * 16);
-                        vr[u][c] = *reinterpret_cast<const uint4*>(vp + c * 128 + r * 16);
+                        kr[u][c] = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(rk, vo + c * 128, so, 0));
+                        vr[u][c] = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(rv, vo + c * 128, so, 0));
                     }
                 }
-                float y[kUnroll][G];
+                float xs[kUnroll][G];
+#pragma unroll
+                for (int u = 0; u < kUnroll; ++u)
+#pragma unroll
+                    for (int h = 0; h < G; ++h) xs[u][h] = lane_dot<BF16, D>(kr[u], qr[h]);
+                // 8-lane sums (every lane of a slot ends with the same bits)
+#pragma unroll
+                for (int u = 0; u < kUnroll; ++u)
+#pragma unroll
+                    for (int h = 0; h < G; ++h) xs[u][h] += dpp_mov<0xB1>(xs[u][h]);   // quad_perm [1,0,3,2]
+#pragma unroll
+                for (int u = 0; u < kUnroll; ++u)
+#pragma unroll
+                    for (int h = 0; h < G; ++h) xs[u][h] += dpp_mov<0x4E>(xs[u][h]);   // quad_perm [2,3,0,1]
+#pragma unroll
+                for (int u = 0; u < kUnroll; ++u)
+#pragma unroll
+                    for (int h = 0; h < G; ++h) xs[u][h] += dpp_mov<0x141>(xs[u][h]);  // row_half_mirror
+
+                // relevance: sum over the slot's heads, then over the token's KV-head slots
 #pragma unroll
                 for (int u = 0; u < kUnroll; ++u) {
                     float rel = 0.f;
 #pragma unroll
-                    for (int h = 0; h < G; ++h) {
-                        const float x = slot_sum(lane_dot<BF16, D>(kr[u], qr[h]));
-                        rel += fabsf(x);
-                        y[u][h] = valid[u] ? x * a.scale_log2 : -INFINITY;
-                    }
-                    if (valid[u] && r == 0) rel_lds[g * kChunkMax + base + u * kSlots + slot] = rel;
+                    for (int h = 0; h < G; ++h) rel += fabsf(xs[u][h]);
+                    if constexpr (HKV >= 2) rel += lane_xor<8>(rel);
+                    if constexpr (HKV >= 4) rel += lane_xor<16>(rel);
+                    if constexpr (HKV >= 8) rel += lane_xor<32>(rel);
+                    if (valid[u] && g == 0 && r == 0 && pos[u] < wedge && rel < a.tau_H)
+                        flag_lds[tb + u * TPI + tk] = 1;
                 }
-                // per-slot running maximum; rescale only when some slot's maximum grows
+
+                float y[kUnroll][G];
+#pragma unroll
+                for (int u = 0; u < kUnroll; ++u)
+#pragma unroll
+                    for (int h = 0; h < G; ++h) y[u][h] = valid[u] ? xs[u][h] * a.scale_log2 : -INFINITY;
 #pragma unroll
                 for (int h = 0; h < G; ++h) {
-                    float mt = m[h];
+                    float mt = st.m[h];
 #pragma unroll
                     for (int u = 0; u < kUnroll; ++u) mt = fmaxf(mt, y[u][h]);
-                    if (__any(mt > m[h])) {
-                        const float sc = (mt > m[h]) ? exp2f(m[h] - mt) : 1.f;
-                        l[h] *= sc;
+                    if (__any(mt > st.m[h])) {
+                        const float sc = (mt > st.m[h]) ? __builtin_amdgcn_exp2f(st.m[h] - mt) : 1.f;
+                        st.l[h] *= sc;
 #pragma unroll
-                        for (int e = 0; e < EL; ++e) acc[h][e] *= sc;
-                        m[h] = mt;
+                        for (int e = 0; e < EL; ++e) st.acc[h][e] *= sc;
+                        st.m[h] = mt;
                     }
                 }
 #pragma unroll
                 for (int u = 0; u < kUnroll; ++u) {
 #pragma unroll
                     for (int h = 0; h < G; ++h) {
-                        const float p = valid[u] ? exp2f(y[u][h] - m[h]) : 0.f;
-                        l[h] += p;
-                        lane_axpy<BF16, D>(acc[h], p, vr[u]);
+                        const float pr = valid[u] ? __builtin_amdgcn_exp2f(y[u][h] - st.m[h]) : 0.f;
+                        st.l[h] += pr;
+                        lane_axpy<BF16, D>(st.acc[h], pr, vr[u]);
                     }
                 }
             }
             __syncthreads();
 
-            // freeze loop over this chunk: relevance summed over KV heads in fixed order
+            // freeze loop over the chunk's flagged tokens (Alg. 1; Eq. 3)
             for (int i = threadIdx.x; i < len; i += blockDim.x) {
-                const int p = pos_lds[i];
-                if (p >= wedge) continue;
-                float sH = 0.f;
-                for (int gg = 0; gg < a.Hkv; ++gg) sH += rel_lds[gg * kChunkMax + i];
-                if (sH < a.tau_H) {
-                    const size_t o = (size_t)b * a.cap + p;
-                    const int c = a.count[o] + 1;
-                    a.count[o] = c;
-                    const int d = a.dur[min(c, a.dur_len - 1)];
-                    if (d >= 1) a.unfreeze[o] = a.t + d;
+                if (!flag_lds[i]) continue;
+                const size_t o = seq_row + pos_lds[i];
+                const int c = a.count[o] + 1;
+                a.count[o] = c;
+                const int d = c < kDurCache ? dur_lds[c] : a.dur[min(c, a.dur_len - 1)];
+                if (d >= 1) a.unfreeze[o] = a.t + d;
+            }
+            __syncthreads();                       // LDS chunk buffers are reused next
+        }
+
+        // merge the waves' states: a fixed tree through LDS (4 -> 2 -> 1 partners)
+#pragma unroll
+        for (int half = kWaves / 2; half >= 1; half >>= 1) {
+            __syncthreads();
+            if (wave >= half && wave < 2 * half) {
+                float* dst = merge_lds + (size_t)(wave - half) * NV * 64 + lane;
+#pragma unroll
+                for (int h = 0; h < G; ++h) {
+                    dst[(2 * h) * 64] = st.m[h];
+                    dst[(2 * h + 1) * 64] = st.l[h];
+#pragma unroll
+                    for (int e = 0; e < EL; ++e) dst[(2 * G + h * EL + e) * 64] = st.acc[h][e];
                 }
             }
             __syncthreads();
-        }
-
-        // merge the 8 slots: common maximum, then sums over lanes r, r+8, ..., r+56
+            if (wave < half) {
+                const float* src = merge_lds + (size_t)wave * NV * 64 + lane;
+                float bm[G], bl[G], bacc[G][EL];
 #pragma unroll
-        for (int h = 0; h < G; ++h) {
-            float mm = m[h];
-            mm = fmaxf(mm, __shfl_xor(mm, 8));
-            mm = fmaxf(mm, __shfl_xor(mm, 16));
-            mm = fmaxf(mm, __shfl_xor(mm, 32));
-            const float sc = (m[h] == -INFINITY) ? 0.f : exp2f(m[h] - mm);
-            float lh = l[h] * sc;
-            lh += __shfl_xor(lh, 8);
-            lh += __shfl_xor(lh, 16);
-            lh += __shfl_xor(lh, 32);
+                for (int h = 0; h < G; ++h) {
+                    bm[h] = src[(2 * h) * 64];
+                    bl[h] = src[(2 * h + 1) * 64];
 #pragma unroll
-            for (int e = 0; e < EL; ++e) {
-                float v = acc[h][e] * sc;
-                v += __shfl_xor(v, 8);
-                v += __shfl_xor(v, 16);
-                v += __shfl_xor(v, 32);
-                acc[h][e] = v;
+                    for (int e = 0; e < EL; ++e) bacc[h][e] = src[(2 * G + h * EL + e) * 64];
+                }
+                fold<BF16, D, G>(st, bm, bl, bacc);
             }
-            m[h] = mm;
-            l[h] = lh;
         }
-        // partial of (workgroup w, sequence b) at slot w + b; slot h writes query head g*G + h
-        const size_t part = (size_t)(w + b);
+        if (wave == 0) {
+            // merge the slots that hold the same KV head (different tokens of an iteration)
 #pragma unroll
-        for (int h = 0; h < G; ++h) {
-            if (slot == h) {
-                const size_t head = part * a.Hq + (size_t)g * G + h;
-                float* dst = a.part_acc + head * D;
+            for (int mask = 8 * HKV; mask < 64; mask <<= 1) {
+                float bm[G], bl[G], bacc[G][EL];
 #pragma unroll
-                for (int e = 0; e < EL; ++e) dst[lane_dim<BF16, D>(r, e)] = acc[h][e];
-                if (r == 0) {
-                    a.part_ml[head * 2 + 0] = m[h];
-                    a.part_ml[head * 2 + 1] = l[h];
+                for (int h = 0; h < G; ++h) {
+                    bm[h] = __shfl_xor(st.m[h], mask);
+                    bl[h] = __shfl_xor(st.l[h], mask);
+#pragma unroll
+                    for (int e = 0; e < EL; ++e) bacc[h][e] = __shfl_xor(st.acc[h][e], mask);
+                }
+                // fold in a fixed order: the lower lane's state first
+                if (lane & mask) {
+#pragma unroll
+                    for (int h = 0; h < G; ++h) {
+                        const float tm = st.m[h], tl = st.l[h];
+                        st.m[h] = bm[h]; bm[h] = tm;
+                        st.l[h] = bl[h]; bl[h] = tl;
+#pragma unroll
+                        for (int e = 0; e < EL; ++e) {
+                            const float ta = st.acc[h][e];
+                            st.acc[h][e] = bacc[h][e];
+                            bacc[h][e] = ta;
+                        }
+                    }
+                }
+                fold<BF16, D, G>(st, bm, bl, bacc);
+            }
+            // partial of (workgroup w, sequence b): slot (token 0, KV head g) writes heads g*G..
+            if (tk == 0) {
+                const size_t part = (size_t)(w + b) * a.Hq + (size_t)g * G;
+#pragma unroll
+                for (int h = 0; h < G; ++h) {
+                    float* dst = a.part_acc + (part + h) * D;
+#pragma unroll
+                    for (int c = 0; c < NC; ++c)
+#pragma unroll
+                        for (int i = 0; i < R::kPerChunk; i += 4) {
+                            const int e = c * R::kPerChunk + i;
+                            *reinterpret_cast<float4*>(dst + c * (128 / R::kElem) + r * R::kPerChunk + i) =
+                                make_float4(st.acc[h][e], st.acc[h][e + 1], st.acc[h][e + 2], st.acc[h][e + 3]);
+                        }
+                    if (r == 0) {
+                        a.part_ml[(part + h) * 2 + 0] = st.m[h];
+                        a.part_ml[(part + h) * 2 + 1] = st.l[h];
+                    }
                 }
             }
         }
-        lo = i1 + seq_off[b];
+        x = sb + i1;
     }
 }
 
-// out[b][h] = sum_s 2^(m_s - M) acc_s / sum_s 2^(m_s - M) l_s over the partial
-// slots of sequence b, in a fixed order.
-template <int D>
-__global__ void __launch_bounds__(256)
-combine_kernel(CombineArgs a) {
-    constexpr int NG = 256 / D;                  // slot groups
-    __shared__ float red_o[256];
-    __shared__ float red_l[256];
-    __shared__ float red_m[256];
-    const int b = blockIdx.x, h = blockIdx.y;
-    const int tid = threadIdx.x;
+// Split combine.  A block owns 64 dims of one query head of one sequence;
+// its 4 slot groups each take every 4th partial slot and the groups' sums are
+// added in a fixed order:
+//   out[b][h][d] = sum_s 2^(m_s - M) acc_s[d] / sum_s 2^(m_s - M) l_s.
+constexpr int kFinishThreads = 256;
+constexpr int kFinishDims = 64;
+constexpr int kSlotGroups = kFinishThreads / kFinishDims;
+constexpr int kSlotUnroll = 4;
+
+__global__ void __launch_bounds__(kFinishThreads)
+finish_kernel(FinishArgs a, int D) {
+    __shared__ float red[kFinishThreads];
+    __shared__ float redl[kFinishThreads];
+    const int per_head = D / kFinishDims;
+    const int bh = blockIdx.x / per_head;                 // b * Hq + h
+    const int d = (blockIdx.x % per_head) * kFinishDims + threadIdx.x % kFinishDims;
+    const int grp = threadIdx.x / kFinishDims;
+    const int b = bh / a.Hq, h = bh % a.Hq;
     const int s0 = a.slot_first[b], s1 = a.slot_end[b];
-    float mx = -INFINITY;
-    for (int s = s0 + tid; s < s1; s += 256) mx = fmaxf(mx, a.part_ml[((size_t)s * a.Hq + h) * 2]);
-    red_m[tid] = mx;
+    // M = max over the slots of m_s (every thread of the block takes part)
+    float M = -INFINITY;
+    for (int k = s0 + (int)threadIdx.x; k < s1; k += kFinishThreads)
+        M = fmaxf(M, a.part_ml[((size_t)k * a.Hq + h) * 2]);
+    red[threadIdx.x] = M;
     __syncthreads();
-    for (int o = 128; o > 0; o >>= 1) {
-        if (tid < o) red_m[tid] = fmaxf(red_m[tid], red_m[tid + o]);
+    for (int o = kFinishThreads / 2; o > 0; o >>= 1) {
+        if ((int)threadIdx.x < o) red[threadIdx.x] = fmaxf(red[threadIdx.x], red[threadIdx.x + o]);
         __syncthreads();
     }
-    const float M = red_m[0];
-    const int grp = tid / D, d = tid % D;
+    M = red[0];
+    __syncthreads();
     float L = 0.f, acc = 0.f;
-#pragma unroll 4
-    for (int s = s0 + grp; s < s1; s += NG) {
-        const size_t head = (size_t)s * a.Hq + h;
-        const float wgt = exp2f(a.part_ml[head * 2] - M);
-        L = fmaf(wgt, a.part_ml[head * 2 + 1], L);
-        acc = fmaf(wgt, a.part_acc[head * D + d], acc);
+    for (int k = s0 + grp; k < s1; k += kSlotGroups * kSlotUnroll) {
+        float mk[kSlotUnroll], lk[kSlotUnroll], ak[kSlotUnroll];
+#pragma unroll
+        for (int u = 0; u < kSlotUnroll; ++u) {
+            const int ks = min(k + u * kSlotGroups, s1 - 1);
+            const size_t head = (size_t)ks * a.Hq + h;
+            mk[u] = a.part_ml[head * 2];
+            lk[u] = a.part_ml[head * 2 + 1];
+            ak[u] = a.part_acc[head * D + d];
+        }
+#pragma unroll
+        for (int u = 0; u < kSlotUnroll; ++u) {
+            if (k + u * kSlotGroups < s1) {
+                const float wgt = __builtin_amdgcn_exp2f(mk[u] - M);
+                L = fmaf(wgt, lk[u], L);
+                acc = fmaf(wgt, ak[u], acc);
+            }
+        }
     }
-    red_o[tid] = acc;
-    red_l[tid] = L;
+    red[threadIdx.x] = acc;
+    redl[threadIdx.x] = L;
     __syncthreads();
     if (grp == 0) {
         float o = 0.f, lt = 0.f;
-        for (int k = 0; k < NG; ++k) { o += red_o[k * D + d]; lt += red_l[k * D + d]; }
-        a.out[((size_t)b * a.Hq + h) * D + d] = o / lt;
+#pragma unroll
+        for (int k = 0; k < kSlotGroups; ++k) {
+            o += red[k * kFinishDims + threadIdx.x];
+            lt += redl[k * kFinishDims + threadIdx.x];
+        }
+        a.out[(size_t)bh * D + d] = o / lt;
     }
 }
 
-size_t lds_bytes(const AttnArgs& a) {
-    return (size_t)(((a.B + 1 + 3) & ~3) + kChunkMax + a.Hkv * kChunkMax) * 4;
-}
+template <bool BF16, int D, int G>
+constexpr int state_floats() { return 2 * G + G * Row<BF16, D>::kPerLane; }
 
 template <bool BF16, int D, int G>
-hipError_t launch_t(const AttnArgs& a, int grid, hipStream_t s) {
-    const size_t lds = lds_bytes(a);
-    hipLaunchKernelGGL((attention_kernel<BF16, D, G>), dim3(grid), dim3(64 * a.Hkv), lds, s, a);
+size_t lds_bytes(const AttnArgs& a) {
+    return (size_t)(((a.B + 1 + 3) & ~3) + kDurCache + kChunk) * 4 + kChunk +
+           (size_t)(kWaves / 2) * state_floats<BF16, D, G>() * 64 * 4;
+}
+
+template <bool BF16, int D, int G, int HKV>
+hipError_t launch_t(const AttnArgs& a, int grid, hipStream_t s, int* occ) {
+    const size_t lds = lds_bytes<BF16, D, G>(a);
+    if (occ)
+        return hipOccupancyMaxActiveBlocksPerMultiprocessor(occ, attention_kernel<BF16, D, G, HKV>,
+                                                            64 * kWaves, lds);
+    hipLaunchKernelGGL((attention_kernel<BF16, D, G, HKV>), dim3(grid), dim3(64 * kWaves), lds, s, a);
     return hipGetLastError();
 }
 
 template <bool BF16, int D, int G>
-hipError_t occupancy_t(const AttnArgs& a, int* blocks) {
-    return hipOccupancyMaxActiveBlocksPerMultiprocessor(blocks, attention_kernel<BF16, D, G>,
-                                                        64 * a.Hkv, lds_bytes(a));
+hipError_t launch_h(const AttnArgs& a, int grid, hipStream_t s, int* occ) {
+    switch (a.Hkv) {
+        case 1: return launch_t<BF16, D, G, 1>(a, grid, s, occ);
+        case 2: return launch_t<BF16, D, G, 2>(a, grid, s, occ);
+        case 4: return launch_t<BF16, D, G, 4>(a, grid, s, occ);
+        case 8: return launch_t<BF16, D, G, 8>(a, grid, s, occ);
+    }
+    return hipErrorInvalidValue;
 }
 
 template <bool BF16, int D>
 hipError_t launch_g(const AttnArgs& a, int group, int grid, hipStream_t s, int* occ) {
     switch (group) {
-        case 1: return occ ? occupancy_t<BF16, D, 1>(a, occ) : launch_t<BF16, D, 1>(a, grid, s);
-        case 2: return occ ? occupancy_t<BF16, D, 2>(a, occ) : launch_t<BF16, D, 2>(a, grid, s);
-        case 4: return occ ? occupancy_t<BF16, D, 4>(a, occ) : launch_t<BF16, D, 4>(a, grid, s);
-        case 8: return occ ? occupancy_t<BF16, D, 8>(a, occ) : launch_t<BF16, D, 8>(a, grid, s);
+        case 1: return launch_h<BF16, D, 1>(a, grid, s, occ);
+        case 2: return launch_h<BF16, D, 2>(a, grid, s, occ);
+        case 4: return launch_h<BF16, D, 4>(a, grid, s, occ);
+        case 8: return launch_h<BF16, D, 8>(a, grid, s, occ);
     }
     return hipErrorInvalidValue;
 }
@@ -452,14 +586,10 @@ hipError_t attention_occupancy(const AttnArgs& a, int dtype_bf16, int head_dim, 
     return dispatch(a, dtype_bf16, head_dim, group, 0, nullptr, blocks_per_cu);
 }
 
-hipError_t launch_combine(const CombineArgs& a, int head_dim, hipStream_t s) {
-    if (head_dim == 128) {
-        hipLaunchKernelGGL(combine_kernel<128>, dim3(a.B, a.Hq), dim3(256), 0, s, a);
-    } else if (head_dim == 64) {
-        hipLaunchKernelGGL(combine_kernel<64>, dim3(a.B, a.Hq), dim3(256), 0, s, a);
-    } else {
-        return hipErrorInvalidValue;
-    }
+hipError_t launch_finish(const FinishArgs& a, int head_dim, hipStream_t s) {
+    if (head_dim % kFinishDims) return hipErrorInvalidValue;
+    const dim3 grid(a.B * a.Hq * (head_dim / kFinishDims));
+    hipLaunchKernelGGL(finish_kernel, grid, dim3(kFinishThreads), 0, s, a, head_dim);
     return hipGetLastError();
 }
 

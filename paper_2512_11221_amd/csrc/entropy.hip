@@ -1,20 +1,22 @@
 // Entropy of the next-token distribution and the recovery ladder (Sec. 3.6).
 //
-// One workgroup per sequence, one pass over the V logits.  Each thread keeps
-// (m, S, T) with S = sum e^(x-m) and T = sum e^(x-m) (x-m) over its logits;
-// the triples are merged across the block, and
+// kEntropySplit workgroups per sequence, one pass over the V logits.  Each
+// thread keeps (m, S, T) with S = sum e^(x-m) and T = sum e^(x-m) (x-m) over
+// its logits; the triples are merged across the block and stored.  The last
+// block of a sequence to finish (a per-sequence ticket) merges the stored
+// triples in block order and forms
 //     H = ln S - T / S          (nats, softmax at temperature 1)
-//     p_max = 1 / S.
-// Thread 0 then updates the sequence's escalation count (one level per
-// consecutive spike step, reset by a calm step) and writes the level that the
-// end-of-step compaction applies: 1 SR, 2 WR, 3 FR; a count above 3 also
-// records a Rewalk Regeneration request.
+//     p_max = 1 / S,
+// then updates the sequence's escalation count (one level per consecutive
+// spike step, reset by a calm step) and writes the level that the end-of-step
+// compaction applies: 1 SR, 2 WR, 3 FR; a count above 3 also records a
+// Rewalk Regeneration request.
 #include "kernels.h"
 
 namespace asrkf {
 namespace {
 
-constexpr int kThreads = 1024;
+constexpr int kThreads = 256;
 
 struct Triple {
     float m, S, T;
@@ -51,21 +53,22 @@ __device__ __forceinline__ Triple merge(const Triple& a, const Triple& b) {
 __global__ void __launch_bounds__(kThreads)
 entropy_kernel(EntropyArgs a) {
     __shared__ Triple part[kThreads / 64];
-    const int b = blockIdx.x;
+    __shared__ int last;
+    const int b = blockIdx.y;
+    const int sp = blockIdx.x;
     const float* x = a.logits + (size_t)b * a.V;
     Triple acc{-INFINITY, 0.f, 0.f};
-    const bool vec = ((reinterpret_cast<uintptr_t>(x) & 15) == 0);
-    int v0 = 0;
-    if (vec) {
-        const int nv = a.V / 4;
-        for (int i = threadIdx.x; i < nv; i += kThreads) {
+    if (((reinterpret_cast<uintptr_t>(x) & 15) == 0) && (a.V % 4 == 0)) {
+        const int n4 = a.V / 4;
+        const int i0 = (int)((int64_t)sp * n4 / kEntropySplit), i1 = (int)((int64_t)(sp + 1) * n4 / kEntropySplit);
+        for (int i = i0 + threadIdx.x; i < i1; i += kThreads) {
             const float4 f = reinterpret_cast<const float4*>(x)[i];
             push(acc, f.x); push(acc, f.y); push(acc, f.z); push(acc, f.w);
         }
-        v0 = nv * 4;
+    } else {
+        const int i0 = (int)((int64_t)sp * a.V / kEntropySplit), i1 = (int)((int64_t)(sp + 1) * a.V / kEntropySplit);
+        for (int i = i0 + threadIdx.x; i < i1; i += kThreads) push(acc, x[i]);
     }
-    for (int i = v0 + threadIdx.x; i < a.V; i += kThreads) push(acc, x[i]);
-
     for (int o = 32; o > 0; o >>= 1) {
         Triple other{__shfl_xor(acc.m, o), __shfl_xor(acc.S, o), __shfl_xor(acc.T, o)};
         acc = merge(acc, other);
@@ -75,29 +78,44 @@ entropy_kernel(EntropyArgs a) {
     if (threadIdx.x == 0) {
         Triple r = part[0];
         for (int w = 1; w < kThreads / 64; ++w) r = merge(r, part[w]);
-        const float H = logf(r.S) - r.T / r.S;
-        const float pmax = 1.f / r.S;
-        a.entropy[b] = H;
-        a.pmax[b] = pmax;
-        int level = 0;
-        if (a.mode == 0) {
-            const bool spike = (H > a.theta_H) || (a.theta_p > 0.f && pmax < a.theta_p);
-            const int esc = spike ? a.escalation[b] + 1 : 0;
-            a.escalation[b] = esc;
-            level = min(esc, 3);
-            if (esc > 3) atomicAdd(a.rr_requests, 1ull);
-        } else if (a.mode >= 1 && a.mode <= 3) {
-            level = a.mode;
-        }
-        a.level[b] = level;
-        if (level > 0) atomicAdd(a.recoveries + level, 1ull);
+        float* dst = a.partial + ((size_t)b * kEntropySplit + sp) * 3;
+        __hip_atomic_store(dst, r.m, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        __hip_atomic_store(dst + 1, r.S, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        __hip_atomic_store(dst + 2, r.T, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        __threadfence();
+        last = (atomicAdd(a.ticket + b, 1) == kEntropySplit - 1);
     }
+    __syncthreads();
+    if (!last || threadIdx.x != 0) return;
+    __threadfence();
+    // the other blocks' triples, read at device scope (they may sit in another XCD's L2)
+    float* src = a.partial + (size_t)b * kEntropySplit * 3;
+    auto ld = [](float* p) { return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT); };
+    Triple r{ld(src), ld(src + 1), ld(src + 2)};
+    for (int k = 1; k < kEntropySplit; ++k) r = merge(r, Triple{ld(src + 3 * k), ld(src + 3 * k + 1), ld(src + 3 * k + 2)});
+    a.ticket[b] = 0;                           // ready for the next step
+    const float H = logf(r.S) - r.T / r.S;
+    const float pmax = 1.f / r.S;
+    a.entropy[b] = H;
+    a.pmax[b] = pmax;
+    int level = 0;
+    if (a.mode == 0) {
+        const bool spike = (H > a.theta_H) || (a.theta_p > 0.f && pmax < a.theta_p);
+        const int esc = spike ? a.escalation[b] + 1 : 0;
+        a.escalation[b] = esc;
+        level = min(esc, 3);
+        if (esc > 3) atomicAdd(a.rr_requests, 1ull);
+    } else if (a.mode >= 1 && a.mode <= 3) {
+        level = a.mode;
+    }
+    a.level[b] = level;
+    if (level > 0) atomicAdd(a.recoveries + level, 1ull);
 }
 
 }  // namespace
 
 hipError_t launch_entropy(const EntropyArgs& a, hipStream_t s) {
-    hipLaunchKernelGGL(entropy_kernel, dim3(a.B), dim3(kThreads), 0, s, a);
+    hipLaunchKernelGGL(entropy_kernel, dim3(kEntropySplit, a.B), dim3(kThreads), 0, s, a);
     return hipGetLastError();
 }
 

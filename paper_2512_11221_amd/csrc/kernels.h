@@ -6,11 +6,11 @@
 
 namespace asrkf {
 
-// Split-K attention: the active lists of all sequences, concatenated, are cut
-// into one contiguous range per workgroup of a fixed grid; every workgroup
-// derives the cut from the active counts on the device (no host round trip).
-// A range is walked in chunks of at most kChunkMax tokens (LDS staging).
-constexpr int kChunkMax = 1024;
+// Split-K attention.  The concatenated active lists of all sequences are cut
+// into one equal contiguous token range per workgroup of a fixed grid
+// (derived on the device from the active counts, no host round trip); the
+// workgroup leaves one partial (m, l, acc) of every query head per sequence
+// its range touches, at slot (workgroup + sequence).
 constexpr int kMaxBatch = 1024;
 
 struct AttnArgs {
@@ -27,7 +27,7 @@ struct AttnArgs {
     int32_t* unfreeze;        // layer base, [B][cap]: U_j
     int32_t* count;           // layer base, [B][cap]: c_j
     const int32_t* dur;       // [dur_len] freeze duration by count (Eq. 3)
-    float* part_acc;          // [grid + B][Hq][D]: partial of (workgroup w, seq b) at slot w + b
+    float* part_acc;          // [grid + B][Hq][D]
     float* part_ml;           // [grid + B][Hq][2]: (max in log2 units, sum)
     int32_t* slot_first;      // [B] first partial slot of each sequence (written)
     int32_t* slot_end;        // [B] one past its last slot (written)
@@ -39,7 +39,8 @@ struct AttnArgs {
     float scale_log2;         // log2(e) / sqrt(D)
 };
 
-struct CombineArgs {
+// Per layer, after the attention: the split combine of Eq. 1.
+struct FinishArgs {
     const float* part_acc;
     const float* part_ml;
     const int32_t* slot_first;
@@ -60,8 +61,12 @@ struct CompactArgs {
     int32_t B, cap, wr_last_N;
 };
 
+constexpr int kEntropySplit = 32;   // workgroups per sequence in the entropy pass
+
 struct EntropyArgs {
     const float* logits;      // [B][V]
+    float* partial;           // [B][kEntropySplit][3] block triples (m, S, T)
+    int32_t* ticket;          // [B] blocks finished; reset by the last one
     int32_t V, B;
     float theta_H, theta_p;
     int32_t mode;             // 0 AUTO, 1..3 forced, 4 none
@@ -77,7 +82,7 @@ hipError_t launch_attention(const AttnArgs& a, int dtype_bf16, int head_dim, int
                             int grid, hipStream_t s);
 hipError_t attention_occupancy(const AttnArgs& a, int dtype_bf16, int head_dim, int group,
                                int* blocks_per_cu);
-hipError_t launch_combine(const CombineArgs& a, int head_dim, hipStream_t s);
+hipError_t launch_finish(const FinishArgs& a, int head_dim, hipStream_t s);
 hipError_t launch_compact(const CompactArgs& a, int n_instances, hipStream_t s);
 hipError_t launch_entropy(const EntropyArgs& a, hipStream_t s);
 

@@ -73,7 +73,7 @@ struct asrkf_ctx {
     int group = 0;
     size_t esz = 0;
     size_t row_bytes = 0;        // one token, all KV heads
-    int grid = 0;                // persistent attention grid (resident workgroups)
+    int grid = 0;                // attention grid (resident workgroups)
     int n_slots = 0;             // partial slots: grid + batch
     int dur_len = 0;
 
@@ -93,6 +93,8 @@ struct asrkf_ctx {
     float* part_acc = nullptr;
     float* part_ml = nullptr;
     int32_t* slot_info = nullptr;   // [2B]: first slot, end slot per sequence
+    float* ent_partial = nullptr;   // [B][kEntropySplit][3]
+    int32_t* ent_ticket = nullptr;  // [B]
     unsigned long long* counters = nullptr;   // [0] listed_total, [1..3] recoveries, [5] rr
 
     std::vector<int32_t> plen_host;
@@ -145,7 +147,7 @@ asrkf_status dev_alloc(asrkf_ctx* ctx, T** p, size_t bytes) {
 void free_all(asrkf_ctx* ctx) {
     void* ptrs[] = {ctx->kpool, ctx->vpool, ctx->unfreeze, ctx->count, ctx->list,
                     ctx->n_active, ctx->plen, ctx->dur, ctx->escalation, ctx->level,
-                    ctx->entropy, ctx->pmax, ctx->part_acc, ctx->part_ml, ctx->slot_info,
+                    ctx->entropy, ctx->pmax, ctx->part_acc, ctx->part_ml, ctx->slot_info, ctx->ent_partial, ctx->ent_ticket,
                     ctx->counters};
     for (void* p : ptrs) if (p) (void)hipFree(p);
     for (auto& ev : ctx->ev_used) { (void)hipEventDestroy(ev.first); (void)hipEventDestroy(ev.second); }
@@ -156,7 +158,8 @@ asrkf_status validate(const asrkf_config* c) {
     if (!c) return fail(ASRKF_EINVAL, "null config");
     if (c->n_layers < 1) return fail(ASRKF_EINVAL, "n_layers must be >= 1");
     if (c->batch < 1 || c->batch > kMaxBatch) return fail(ASRKF_EINVAL, "batch must be in 1..%d", kMaxBatch);
-    if (c->n_kv_heads < 1 || c->n_kv_heads > 8) return fail(ASRKF_EINVAL, "n_kv_heads must be in 1..8");
+    if (c->n_kv_heads != 1 && c->n_kv_heads != 2 && c->n_kv_heads != 4 && c->n_kv_heads != 8)
+        return fail(ASRKF_EINVAL, "n_kv_heads must be 1, 2, 4 or 8");
     if (c->n_q_heads < c->n_kv_heads || c->n_q_heads % c->n_kv_heads)
         return fail(ASRKF_EINVAL, "n_q_heads must be a multiple of n_kv_heads");
     const int g = c->n_q_heads / c->n_kv_heads;
@@ -170,6 +173,12 @@ asrkf_status validate(const asrkf_config* c) {
     if (isnan(c->entropy_spike) || isnan(c->conf_drop)) return fail(ASRKF_EINVAL, "NaN threshold");
     if (c->dtype != ASRKF_BF16 && c->dtype != ASRKF_F32) return fail(ASRKF_EINVAL, "unknown dtype");
     if (c->spill_min_D != 0) return fail(ASRKF_EINVAL, "spill mode is not available in this build");
+    {
+        const int64_t row = (int64_t)c->n_kv_heads * c->head_dim * (c->dtype == ASRKF_BF16 ? 2 : 4);
+        const int64_t cap = ((int64_t)c->max_ctx + 1 + 63) / 64 * 64;
+        if (cap * row >= ((int64_t)1 << 31))
+            return fail(ASRKF_EINVAL, "max_ctx too large: one sequence's cache must stay below 2 GiB per layer");
+    }
     return ASRKF_OK;
 }
 
@@ -218,7 +227,11 @@ asrkf_status asrkf_init(const asrkf_config* cfg, asrkf_ctx** out) {
         int per_cu = 0;
         e = attention_occupancy(probe, c.dtype == ASRKF_BF16, c.head_dim, ctx->group, &per_cu);
         if (e != hipSuccess) { delete ctx; return hip_fail(nullptr, e, "hipOccupancyMaxActiveBlocksPerMultiprocessor"); }
-        ctx->grid = std::max(1, per_cu) * prop.multiProcessorCount;
+        if (per_cu < 1) {
+            delete ctx;
+            return fail(ASRKF_EINVAL, "attention workgroup does not fit on a CU for this shape");
+        }
+        ctx->grid = per_cu * prop.multiProcessorCount;
     }
     ctx->n_slots = ctx->grid + c.batch;
     ctx->dur_len = c.max_ctx + 2;
@@ -245,6 +258,8 @@ asrkf_status asrkf_init(const asrkf_config* cfg, asrkf_ctx** out) {
     ALLOC(part_acc, (size_t)ctx->n_slots * c.n_q_heads * c.head_dim * 4);
     ALLOC(part_ml, (size_t)ctx->n_slots * c.n_q_heads * 2 * 4);
     ALLOC(slot_info, (size_t)c.batch * 2 * 4);
+    ALLOC(ent_partial, (size_t)c.batch * kEntropySplit * 3 * 4);
+    ALLOC(ent_ticket, (size_t)c.batch * 4);
     ALLOC(counters, 8 * sizeof(unsigned long long));
 #undef ALLOC
 
@@ -263,6 +278,7 @@ asrkf_status asrkf_init(const asrkf_config* cfg, asrkf_ctx** out) {
     INIT(hipMemset(ctx->level, 0, (size_t)c.batch * 4));
     INIT(hipMemset(ctx->entropy, 0, (size_t)c.batch * 4));
     INIT(hipMemset(ctx->pmax, 0, (size_t)c.batch * 4));
+    INIT(hipMemset(ctx->ent_ticket, 0, (size_t)c.batch * 4));
     INIT(hipMemset(ctx->counters, 0, 8 * sizeof(unsigned long long)));
     INIT(hipMemcpy(ctx->dur, table.data(), table.size() * 4, hipMemcpyHostToDevice));
     INIT(hipDeviceSynchronize());
@@ -390,15 +406,15 @@ asrkf_status asrkf_decode_step(asrkf_ctx* ctx, int32_t layer, const void* q, con
         ctx->ev_used.push_back(ev);
     }
 
-    CombineArgs cb{};
-    cb.part_acc = ctx->part_acc;
-    cb.part_ml = ctx->part_ml;
-    cb.slot_first = ctx->slot_info;
-    cb.slot_end = ctx->slot_info + c.batch;
-    cb.out = out;
-    cb.B = c.batch;
-    cb.Hq = c.n_q_heads;
-    HIP_OK(ctx, launch_combine(cb, c.head_dim, s));
+    FinishArgs f{};
+    f.part_acc = ctx->part_acc;
+    f.part_ml = ctx->part_ml;
+    f.slot_first = a.slot_first;
+    f.slot_end = a.slot_end;
+    f.out = out;
+    f.B = c.batch;
+    f.Hq = c.n_q_heads;
+    HIP_OK(ctx, launch_finish(f, c.head_dim, s));
 
     ctx->next_layer = layer + 1;
     ctx->last_stream = s;
@@ -418,6 +434,8 @@ asrkf_status asrkf_restore(asrkf_ctx* ctx, const float* logits, asrkf_recover mo
     if (logits) {
         EntropyArgs e{};
         e.logits = logits;
+        e.partial = ctx->ent_partial;
+        e.ticket = ctx->ent_ticket;
         e.V = c.vocab;
         e.B = c.batch;
         e.theta_H = c.entropy_spike;
