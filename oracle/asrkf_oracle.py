@@ -79,29 +79,53 @@ def attention(q, K, V):
     q: [Hq][D]; K, V: [n][Hkv][D].  Query head h uses KV head h // (Hq/Hkv).
     Returns [Hq][D] float64: softmax(q_h K^T / sqrt(D)) V per head."""
     q = np.asarray(q, dtype=np.float64)
-    K = np.asarray(K, dtype=np.float64)
-    V = np.asarray(V, dtype=np.float64)
     Hq, D = q.shape
     group = Hq // K.shape[1]
     out = np.zeros((Hq, D))
-    for h in range(Hq):
-        g = h // group
-        logits = K[:, g, :] @ q[h] / np.sqrt(D)
-        w = np.exp(logits - logits.max())
-        out[h] = (w / w.sum()) @ V[:, g, :]
+    for g in range(K.shape[1]):
+        Kg = np.ascontiguousarray(K[:, g, :], dtype=np.float64)
+        Vg = np.ascontiguousarray(V[:, g, :], dtype=np.float64)
+        for h in range(g * group, (g + 1) * group):
+            logits = Kg @ q[h] / np.sqrt(D)
+            w = np.exp(logits - logits.max())
+            out[h] = (w / w.sum()) @ Vg
     return out
 
 
 def relevance(q, K):
     """Eq. 2: s_j = (1/H) sum_h |q_h . K_j^(h)| for every row j of K, H = Hq."""
     q = np.asarray(q, dtype=np.float64)
-    K = np.asarray(K, dtype=np.float64)
     Hq = q.shape[0]
     group = Hq // K.shape[1]
     s = np.zeros(K.shape[0])
-    for h in range(Hq):
-        s += np.abs(K[:, h // group, :] @ q[h])
+    for g in range(K.shape[1]):
+        Kg = np.ascontiguousarray(K[:, g, :], dtype=np.float64)
+        for h in range(g * group, (g + 1) * group):
+            s += np.abs(Kg @ q[h])
     return s / Hq
+
+
+def attend_rows(q, Kh, Vh):
+    """Eq. 1 and Eq. 2 together over rows given per KV head: Kh[g], Vh[g] are
+    [n][D] arrays of the same n tokens.  The G query heads of a KV head are
+    taken together as one matrix product, so each KV head's rows are read once;
+    the results equal attention() and relevance() up to summation order."""
+    q = np.asarray(q, dtype=np.float64)
+    Hq, D = q.shape
+    group = Hq // len(Kh)
+    out = np.zeros((Hq, D))
+    s = np.zeros(len(Kh[0]))
+    for g in range(len(Kh)):
+        Kg = np.asarray(Kh[g], dtype=np.float64)
+        Vg = np.asarray(Vh[g], dtype=np.float64)
+        heads = slice(g * group, (g + 1) * group)
+        X = Kg @ q[heads].T                        # [n][G]: q_h . k_j
+        for i in range(group):
+            s += np.abs(X[:, i])
+        logits = X / np.sqrt(D)
+        W = np.exp(logits - logits.max(axis=0))
+        out[heads] = (W / W.sum(axis=0)).T @ Vg
+    return out, s / Hq
 
 
 # ---------------------------------------------------------------------------
@@ -141,17 +165,21 @@ class StepRecord:
 
 class Instance:
     """Token states of one (layer, sequence): active cache A, frozen storage F,
-    per-token detection count c_j and freeze timer d_j (Algorithm 1 REQUIRE)."""
+    per-token detection count c_j and freeze timer d_j (Algorithm 1 REQUIRE).
+    The cached pairs are kept KV-head major, [Hkv][position][D], in float64."""
 
     def __init__(self, K_prompt, V_prompt, window_K, tau, k_soft, capacity=None):
-        K_prompt = np.asarray(K_prompt, dtype=np.float64)
-        V_prompt = np.asarray(V_prompt, dtype=np.float64)
+        K_prompt = np.asarray(K_prompt)
+        V_prompt = np.asarray(V_prompt)
         P, Hkv, D = K_prompt.shape
         cap = capacity if capacity is not None else P + 4096
-        self.K = np.zeros((cap, Hkv, D))
-        self.V = np.zeros((cap, Hkv, D))
-        self.K[:P] = K_prompt
-        self.V[:P] = V_prompt
+        # cached pairs, KV-head major: [Hkv][position][D]
+        self.K = np.zeros((Hkv, cap, D))
+        self.V = np.zeros((Hkv, cap, D))
+        self._rows_k = np.empty((Hkv, cap, D))     # the attended rows of one step
+        self._rows_v = np.empty((Hkv, cap, D))
+        self.K[:, :P] = K_prompt.transpose(1, 0, 2)
+        self.V[:, :P] = V_prompt.transpose(1, 0, 2)
         self.n = P
         self.window_K = int(window_K)
         self.tau = float(tau)
@@ -173,8 +201,8 @@ class Instance:
         """One generation step for this layer (Algorithm 1, freeze and timer loops)."""
         # the new token's KV joins the active cache
         j_new = self.n
-        self.K[j_new] = k_new
-        self.V[j_new] = v_new
+        self.K[:, j_new] = k_new
+        self.V[:, j_new] = v_new
         self.count[j_new] = 0
         self.timer[j_new] = 0
         self.frozen[j_new] = False
@@ -182,8 +210,11 @@ class Instance:
 
         # Attn(Q_i, A) and relevance s_j for j in A
         A = self.active_positions()
-        out = attention(q, self.K[A], self.V[A])
-        s = relevance(q, self.K[A])
+        n = len(A)
+        for g in range(self.K.shape[0]):
+            np.take(self.K[g], A, axis=0, out=self._rows_k[g, :n], mode="clip")
+            np.take(self.V[g], A, axis=0, out=self._rows_v[g, :n], mode="clip")
+        out, s = attend_rows(q, self._rows_k[:, :n], self._rows_v[:, :n])
         self.freeze_loop(A, s)
         self.timer_loop()
         return StepRecord(out, A, s)

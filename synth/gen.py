@@ -246,16 +246,20 @@ def hh_mask(w, layer, seq, p0, p1):
     return (z >> U64(11)) < thr
 
 
-def _gauss_rows(key, p0, p1, width, attempts=None):
+def _gauss_rows(key, p0, p1, width, attempts=None, block=1024):
     n = p1 - p0
-    ctr = (np.arange(p0, p1, dtype=U64)[:, None] * U64(width)
-           + np.arange(width, dtype=U64)[None, :])
-    out = gauss(draw(key, ctr))
+    out = np.empty((n, width), dtype=np.float32)
+    cols = np.arange(width, dtype=U64)[None, :]
+    for r0 in range(p0, p1, block):            # row blocks keep the temporaries small
+        r1 = min(p1, r0 + block)
+        ctr = np.arange(r0, r1, dtype=U64)[:, None] * U64(width) + cols
+        out[r0 - p0:r1 - p0] = gauss(draw(key, ctr))
     if attempts is not None:
         a = np.asarray(attempts[p0:p1])
         for r in np.nonzero(a)[0]:
-            out[r] = gauss(draw(_row_key(key, int(a[r])), ctr[r]))
-    return out.reshape(n, width)
+            ctr = U64(p0 + int(r)) * U64(width) + cols[0]
+            out[r] = gauss(draw(_row_key(key, int(a[r])), ctr))
+    return out
 
 
 def kv_rows(w, layer, seq, p0, p1, attempts=None):

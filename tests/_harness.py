@@ -229,3 +229,80 @@ def compare_instance(gpu_recs, ora_recs, check_out=True):
             rel = np.linalg.norm(g["out"] - ref) / max(np.linalg.norm(ref), 1e-30)
             assert rel <= RTOL_NORM, (t, rel)
     return worst
+
+
+def run_gpu_device(w, instances, record_steps, seqs_for_entropy=None):
+    """Run a large workload exactly as the bench does (device-generated inputs,
+    the library's own launch configuration).  Returns per instance the attention
+    output of every step and the token states at ``record_steps``; per sequence
+    the entropy monitor of every step."""
+    import torch
+    import paper_2512_11221_amd as A
+    from synth.device import DeviceGen
+
+    L, B, Hq, Hkv, D = w.n_layers, w.batch, w.n_q_heads, w.n_kv_heads, w.head_dim
+    tdt = torch.bfloat16 if w.dtype == "bf16" else torch.float32
+    cfg = A.make_config(L, B, Hq, Hkv, D, w.max_ctx, w.window_K, w.tau, w.k_soft, w.vocab,
+                        entropy_spike=w.entropy_spike, conf_drop=w.conf_drop,
+                        wr_last_N=w.wr_last_N, dtype=w.dtype)
+    ctx = A.asrkf_init(cfg)
+    outs = {key: [] for key in instances}
+    states = {key: {} for key in instances}
+    ent = {b: [] for b in (seqs_for_entropy or range(B))}
+    try:
+        dg = DeviceGen(w)
+        Pmax = max(w.prefill)
+        sk = torch.empty(Pmax * Hkv * D, dtype=tdt, device="cuda")
+        sv = torch.empty_like(sk)
+        for l in range(L):
+            for b in range(B):
+                dg.kv_rows(l, b, 0, w.prefill[b], sk, sv)
+                A.asrkf_prefill(ctx, l, b, sk, sv, w.prefill[b])
+        torch.cuda.synchronize()
+        del sk, sv
+        S = w.steps
+        Q = torch.empty((S, L, B, Hq, D), dtype=tdt, device="cuda")
+        Kn = torch.empty((S, L, B, Hkv, D), dtype=tdt, device="cuda")
+        Vn = torch.empty_like(Kn)
+        LG = torch.empty((S, B, w.vocab), dtype=torch.float32, device="cuda")
+        dg.q(1, S, Q)
+        dg.new_kv(1, S, Kn, Vn)
+        dg.logits(1, S, LG)
+        out = torch.empty((L, B, Hq, D), dtype=torch.float32, device="cuda")
+        for t in range(1, S + 1):
+            for l in range(L):
+                A.asrkf_decode_step(ctx, l, Q[t - 1, l], Kn[t - 1, l], Vn[t - 1, l], out[l])
+            A.asrkf_restore(ctx, LG[t - 1], A.AUTO)
+            torch.cuda.synchronize()
+            for (l, b) in instances:
+                outs[(l, b)].append(out[l, b].cpu().numpy())
+                if t in record_steps:
+                    st = A.asrkf_get_state(ctx, l, b, w.max_ctx)
+                    st["t"] = t
+                    states[(l, b)][t] = st
+            for b in ent:
+                ent[b].append(A.asrkf_get_seq(ctx, b))
+    finally:
+        A.asrkf_destroy(ctx)
+    return outs, states, ent
+
+
+def compare_sampled(w, inp, instances, outs, states, record_steps):
+    """Oracle on the sampled instances over every step: outputs each step within
+    the acceptance bound, states at record_steps bit-exact."""
+    worst = 0.0
+    for (l, b) in instances:
+        ora = run_oracle(w, inp, [(l, b)], record=lambda t: True)[(l, b)]
+        for o in ora:
+            t = o["t"]
+            g = outs[(l, b)][t - 1]
+            err = np.abs(g.astype(np.float64) - o["out"])
+            worst = max(worst, float(err.max()))
+            assert err.max() <= ATOL, (l, b, t, float(err.max()))
+            rel = np.linalg.norm(g - o["out"]) / max(np.linalg.norm(o["out"]), 1e-30)
+            assert rel <= RTOL_NORM, (l, b, t, rel)
+            if t in record_steps:
+                gs = states[(l, b)][t]
+                gs["out"] = g
+                compare_instance([gs], [o], check_out=False)
+    return worst

@@ -159,6 +159,14 @@ def test_attention_special_cases():
                                atol=1e-13)
 
 
+def test_fused_pass_equals_the_definitions():
+    Hq, Hkv, D, n = 8, 2, 16, 41
+    q, K, V = _rand((Hq, D), 21), _rand((n, Hkv, D), 22), _rand((n, Hkv, D), 23)
+    out, s = oracle.attend_rows(q, [K[:, g] for g in range(Hkv)], [V[:, g] for g in range(Hkv)])
+    np.testing.assert_allclose(out, oracle.attention(q, K, V), rtol=1e-13, atol=1e-14)
+    np.testing.assert_allclose(s, oracle.relevance(q, K), rtol=1e-13, atol=1e-14)
+
+
 def test_freezing_nothing_is_dense_attention():
     """tau below every score: nothing is flagged, every step attends all tokens."""
     Hq, Hkv, D, P, steps = 4, 2, 8, 20, 6
