@@ -30,9 +30,31 @@ def parse():
     ap.add_argument("--workload", choices=sorted(WORKLOADS), default="32layer")
     ap.add_argument("--cpu-seconds", type=float, default=15.0,
                     help="budget of the oracle sample (0 disables the cpu_baseline leg)")
-    ap.add_argument("--traffic-json", default=os.path.join(ROOT, "profiles", "attention_traffic.json"),
-                    help="HBM bytes per launch measured with rocprofv3 counters, if present")
+    ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",
+                    help="after the run, one plain device copy of BYTES (counter calibration)")
     return ap.parse_args()
+
+
+TRAFFIC_SUMMARY = os.path.join(ROOT, "profiles", "attention_traffic_llama3-8b-32layer.md")
+ATTENTION_SOURCE = os.path.join(ROOT, "paper_2512_11221_amd", "csrc", "attention.hip")
+
+
+def measured_traffic(workload, steps, warmup):
+    """HBM bytes per attention launch from the committed rocprofv3 counter
+    summary, if it was taken on this workload, these steps and this kernel
+    source; otherwise None."""
+    import hashlib
+    import re
+    if not os.path.exists(TRAFFIC_SUMMARY):
+        return None
+    text = open(TRAFFIC_SUMMARY).read()
+    fields = dict(re.findall(r"^- (\w+): `([^`]*)`", text, flags=re.M))
+    with open(ATTENTION_SOURCE, "rb") as f:
+        sha = hashlib.sha256(f.read()).hexdigest()
+    if (fields.get("workload") != workload or fields.get("attention_source_sha256") != sha
+            or fields.get("steps") != str(steps) or fields.get("warmup") != str(warmup)):
+        return None
+    return float(fields["traffic_bytes_per_launch"])
 
 
 def cpu_baseline(w, budget_s):
@@ -130,19 +152,21 @@ def main():
     elapsed = time.perf_counter() - t0
     st = A.asrkf_stats(ctx)
     A.asrkf_destroy(ctx)
+    del Q, Kn, Vn, LG, out
 
     attended = st["attended_total"]
     bytes_per_token = w.kv_bytes_per_token()          # K + V of one token, one layer
     algo_bytes = bytes_per_token * attended + 4 * w.vocab * B * K
     attn_s = st["attn_kernel_ms"] / 1e3
     achieved = bytes_per_token * attended / attn_s / 1e9
-    traffic = None
-    if os.path.exists(args.traffic_json):
-        with open(args.traffic_json) as f:
-            tj = json.load(f)
-        if tj.get("workload") == w.name:
-            traffic = tj.get("bytes_per_launch")
-    total_positions = sum(p + W + K for p in w.prefill) * L
+    traffic = measured_traffic(w.name, K, W)
+    if args.copy_calibration > 0:
+        src = torch.empty(args.copy_calibration, dtype=torch.uint8, device="cuda")
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
     line = {
         "metric": "active-KV tokens/s per decode step + achieved HBM GB/s vs peak, 8B shape",
         "value": attended / elapsed,
@@ -167,7 +191,8 @@ def main():
         "compression_after_run": st["compression"],
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": PEAK_HBM_GBS, "unit": "GB/s",
                      "frac": achieved / PEAK_HBM_GBS, "traffic": traffic,
-                     "kernel": "attention_kernel<bf16,128,4>",
+                     "kernel": "attention_kernel<bf16, D=128, G=4, Hkv=8>",
+                     "algorithmic_unit": f"{bytes_per_token} B per attended token-layer (K + V rows)",
                      "launches": st["attn_launches"],
                      "avg_launch_us": 1e3 * st["attn_kernel_ms"] / max(1, st["attn_launches"]),
                      "algorithmic_bytes_per_launch": bytes_per_token * attended
