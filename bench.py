@@ -30,6 +30,8 @@ def parse():
     ap.add_argument("--workload", choices=sorted(WORKLOADS), default="32layer")
     ap.add_argument("--cpu-seconds", type=float, default=15.0,
                     help="budget of the oracle sample (0 disables the cpu_baseline leg)")
+    ap.add_argument("--layers", type=int, default=0,
+                    help="run only the first N layers of the workload (counter runs); 0 = all")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",
                     help="after the run, one plain device copy of BYTES (counter calibration)")
     return ap.parse_args()
@@ -42,7 +44,9 @@ ATTENTION_SOURCE = os.path.join(ROOT, "paper_2512_11221_amd", "csrc", "attention
 def measured_traffic(workload, steps, warmup):
     """HBM bytes per attention launch from the committed rocprofv3 counter
     summary, if it was taken on this workload, these steps and this kernel
-    source; otherwise None."""
+    source; otherwise None.  The summary may come from a run of the first
+    layer only: every attention launch covers one layer of the whole batch,
+    so the launches of that run have the same shape as the full run's."""
     import hashlib
     import re
     if not os.path.exists(TRAFFIC_SUMMARY):
@@ -54,7 +58,7 @@ def measured_traffic(workload, steps, warmup):
     if (fields.get("workload") != workload or fields.get("attention_source_sha256") != sha
             or fields.get("steps") != str(steps) or fields.get("warmup") != str(warmup)):
         return None
-    return float(fields["traffic_bytes_per_launch"])
+    return float(fields["traffic_bytes_per_launch"]), fields.get("layers", "all")
 
 
 def cpu_baseline(w, budget_s):
@@ -104,6 +108,8 @@ def main():
     torch.cuda.set_device(0)
     W, K = args.warmup, args.steps
     w = getattr(gen, WORKLOADS[args.workload])(steps=W + K)
+    if args.layers:
+        w = w.replace(n_layers=min(args.layers, w.n_layers))
     L, B, Hq, Hkv, D = w.n_layers, w.batch, w.n_q_heads, w.n_kv_heads, w.head_dim
     tdt = torch.bfloat16 if w.dtype == "bf16" else torch.float32
 
@@ -160,6 +166,7 @@ def main():
     attn_s = st["attn_kernel_ms"] / 1e3
     achieved = bytes_per_token * attended / attn_s / 1e9
     traffic = measured_traffic(w.name, K, W)
+    traffic, traffic_layers = traffic if traffic else (None, None)
     if args.copy_calibration > 0:
         src = torch.empty(args.copy_calibration, dtype=torch.uint8, device="cuda")
         dst = torch.empty_like(src)
@@ -191,6 +198,7 @@ def main():
         "compression_after_run": st["compression"],
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": PEAK_HBM_GBS, "unit": "GB/s",
                      "frac": achieved / PEAK_HBM_GBS, "traffic": traffic,
+                     "traffic_run_layers": traffic_layers,
                      "kernel": "attention_kernel<bf16, D=128, G=4, Hkv=8>",
                      "algorithmic_unit": f"{bytes_per_token} B per attended token-layer (K + V rows)",
                      "launches": st["attn_launches"],

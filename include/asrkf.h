@@ -137,8 +137,9 @@ asrkf_status asrkf_stats(asrkf_ctx* ctx, asrkf_stats_t* out);
  * attention timing).  Waits for all queued work of the context. */
 asrkf_status asrkf_stats_reset(asrkf_ctx* ctx);
 
-/* Record HIP events around every attention launch (enable != 0) so that
- * asrkf_stats reports the kernel's summed duration.  Host-side switch. */
+/* Have every attention launch record a pair of HIP events in its own
+ * dispatch (enable != 0), so that asrkf_stats reports the kernel's summed
+ * execution time.  Host-side switch. */
 asrkf_status asrkf_set_timing(asrkf_ctx* ctx, int32_t enable);
 
 /* Token states of one (layer, sequence) after the last completed step t

@@ -530,46 +530,55 @@ size_t lds_bytes(const AttnArgs& a) {
            (size_t)(kWaves / 2) * state_floats<BF16, D, G>() * 64 * 4;
 }
 
+// Timing events, when given, are recorded by the dispatch itself, so they
+// bracket the kernel's execution and not the queue work around it.
+struct Launch {
+    int grid;
+    hipStream_t stream;
+    hipEvent_t start, stop;
+    int* occ;                       // non-null: report occupancy instead
+};
+
 template <bool BF16, int D, int G, int HKV>
-hipError_t launch_t(const AttnArgs& a, int grid, hipStream_t s, int* occ) {
+hipError_t launch_t(const AttnArgs& a, const Launch& l) {
     const size_t lds = lds_bytes<BF16, D, G>(a);
-    if (occ)
-        return hipOccupancyMaxActiveBlocksPerMultiprocessor(occ, attention_kernel<BF16, D, G, HKV>,
-                                                            64 * kWaves, lds);
-    hipLaunchKernelGGL((attention_kernel<BF16, D, G, HKV>), dim3(grid), dim3(64 * kWaves), lds, s, a);
-    return hipGetLastError();
+    auto k = attention_kernel<BF16, D, G, HKV>;
+    if (l.occ) return hipOccupancyMaxActiveBlocksPerMultiprocessor(l.occ, k, 64 * kWaves, lds);
+    AttnArgs arg = a;
+    void* args[] = {&arg};
+    return hipExtLaunchKernel(reinterpret_cast<const void*>(k), dim3(l.grid), dim3(64 * kWaves),
+                              args, lds, l.stream, l.start, l.stop, 0);
 }
 
 template <bool BF16, int D, int G>
-hipError_t launch_h(const AttnArgs& a, int grid, hipStream_t s, int* occ) {
+hipError_t launch_h(const AttnArgs& a, const Launch& l) {
     switch (a.Hkv) {
-        case 1: return launch_t<BF16, D, G, 1>(a, grid, s, occ);
-        case 2: return launch_t<BF16, D, G, 2>(a, grid, s, occ);
-        case 4: return launch_t<BF16, D, G, 4>(a, grid, s, occ);
-        case 8: return launch_t<BF16, D, G, 8>(a, grid, s, occ);
+        case 1: return launch_t<BF16, D, G, 1>(a, l);
+        case 2: return launch_t<BF16, D, G, 2>(a, l);
+        case 4: return launch_t<BF16, D, G, 4>(a, l);
+        case 8: return launch_t<BF16, D, G, 8>(a, l);
     }
     return hipErrorInvalidValue;
 }
 
 template <bool BF16, int D>
-hipError_t launch_g(const AttnArgs& a, int group, int grid, hipStream_t s, int* occ) {
+hipError_t launch_g(const AttnArgs& a, int group, const Launch& l) {
     switch (group) {
-        case 1: return launch_h<BF16, D, 1>(a, grid, s, occ);
-        case 2: return launch_h<BF16, D, 2>(a, grid, s, occ);
-        case 4: return launch_h<BF16, D, 4>(a, grid, s, occ);
-        case 8: return launch_h<BF16, D, 8>(a, grid, s, occ);
+        case 1: return launch_h<BF16, D, 1>(a, l);
+        case 2: return launch_h<BF16, D, 2>(a, l);
+        case 4: return launch_h<BF16, D, 4>(a, l);
+        case 8: return launch_h<BF16, D, 8>(a, l);
     }
     return hipErrorInvalidValue;
 }
 
-hipError_t dispatch(const AttnArgs& a, int dtype_bf16, int head_dim, int group, int grid,
-                    hipStream_t s, int* occ) {
+hipError_t dispatch(const AttnArgs& a, int dtype_bf16, int head_dim, int group, const Launch& l) {
     if (dtype_bf16) {
-        if (head_dim == 128) return launch_g<true, 128>(a, group, grid, s, occ);
-        if (head_dim == 64) return launch_g<true, 64>(a, group, grid, s, occ);
+        if (head_dim == 128) return launch_g<true, 128>(a, group, l);
+        if (head_dim == 64) return launch_g<true, 64>(a, group, l);
     } else {
-        if (head_dim == 128) return launch_g<false, 128>(a, group, grid, s, occ);
-        if (head_dim == 64) return launch_g<false, 64>(a, group, grid, s, occ);
+        if (head_dim == 128) return launch_g<false, 128>(a, group, l);
+        if (head_dim == 64) return launch_g<false, 64>(a, group, l);
     }
     return hipErrorInvalidValue;
 }
@@ -577,13 +586,13 @@ hipError_t dispatch(const AttnArgs& a, int dtype_bf16, int head_dim, int group, 
 }  // namespace
 
 hipError_t launch_attention(const AttnArgs& a, int dtype_bf16, int head_dim, int group,
-                            int grid, hipStream_t s) {
-    return dispatch(a, dtype_bf16, head_dim, group, grid, s, nullptr);
+                            int grid, hipStream_t s, hipEvent_t start, hipEvent_t stop) {
+    return dispatch(a, dtype_bf16, head_dim, group, Launch{grid, s, start, stop, nullptr});
 }
 
 hipError_t attention_occupancy(const AttnArgs& a, int dtype_bf16, int head_dim, int group,
                                int* blocks_per_cu) {
-    return dispatch(a, dtype_bf16, head_dim, group, 0, nullptr, blocks_per_cu);
+    return dispatch(a, dtype_bf16, head_dim, group, Launch{0, nullptr, nullptr, nullptr, blocks_per_cu});
 }
 
 hipError_t launch_finish(const FinishArgs& a, int head_dim, hipStream_t s) {

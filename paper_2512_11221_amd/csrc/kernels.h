@@ -2,6 +2,7 @@
 #pragma once
 
 #include <hip/hip_runtime.h>
+#include <hip/hip_ext.h>
 #include <stdint.h>
 
 namespace asrkf {
@@ -78,8 +79,9 @@ struct EntropyArgs {
     unsigned long long* rr_requests;
 };
 
+// start/stop (may be null) are recorded by the kernel's own dispatch.
 hipError_t launch_attention(const AttnArgs& a, int dtype_bf16, int head_dim, int group,
-                            int grid, hipStream_t s);
+                            int grid, hipStream_t s, hipEvent_t start, hipEvent_t stop);
 hipError_t attention_occupancy(const AttnArgs& a, int dtype_bf16, int head_dim, int group,
                                int* blocks_per_cu);
 hipError_t launch_finish(const FinishArgs& a, int head_dim, hipStream_t s);

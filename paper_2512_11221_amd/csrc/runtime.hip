@@ -398,13 +398,10 @@ asrkf_status asrkf_decode_step(asrkf_ctx* ctx, int32_t layer, const void* q, con
             HIP_OK(ctx, hipEventCreate(&ev.first));
             HIP_OK(ctx, hipEventCreate(&ev.second));
         }
-        HIP_OK(ctx, hipEventRecord(ev.first, s));
     }
-    HIP_OK(ctx, launch_attention(a, c.dtype == ASRKF_BF16, c.head_dim, ctx->group, ctx->grid, s));
-    if (ctx->timing) {
-        HIP_OK(ctx, hipEventRecord(ev.second, s));
-        ctx->ev_used.push_back(ev);
-    }
+    HIP_OK(ctx, launch_attention(a, c.dtype == ASRKF_BF16, c.head_dim, ctx->group, ctx->grid, s,
+                                 ev.first, ev.second));
+    if (ctx->timing) ctx->ev_used.push_back(ev);
 
     FinishArgs f{};
     f.part_acc = ctx->part_acc;
