@@ -43,7 +43,8 @@ typedef enum {
     ASRKF_ENOMEM = -2,     /* device or pinned host allocation failed */
     ASRKF_EHIP = -3,       /* HIP runtime error; context poisoned */
     ASRKF_ESTATE = -4,     /* call out of order, or context poisoned */
-    ASRKF_ECAPACITY = -5   /* a sequence would exceed max_ctx positions */
+    ASRKF_ECAPACITY = -5   /* a sequence would exceed max_ctx positions, or (spill
+                              mode) needed more than device_rows device rows */
 } asrkf_status;
 
 typedef enum { ASRKF_BF16 = 0, ASRKF_F32 = 1 } asrkf_dtype;
@@ -72,7 +73,19 @@ typedef struct {
     float   conf_drop;       /* theta_p on the top probability; <= 0 disables */
     int32_t wr_last_N;       /* Window Reset span in positions; <= 0 means 4 * window_K */
     asrkf_dtype dtype;       /* storage type of q, k, v */
-    int32_t spill_min_D;     /* 0: frozen KV stays in HBM (resident mode) */
+    int32_t spill_min_D;     /* 0: resident mode, frozen KV stays in HBM and only leaves
+                                the active list.  >= 1: spill mode (Sec. 3.2, frozen KV
+                                moved off the GPU): a token frozen for d >= spill_min_D
+                                steps gives up its device row; its K and V rows are copied
+                                once into a pinned host store and copied back into a free
+                                device row at the end of the step before it attends again
+                                (timer or recovery).  All copies run on a library stream
+                                and are ordered before the attention that reads them. */
+    int32_t device_rows;     /* spill mode: device KV rows per (layer, sequence), 0 means
+                                max_ctx + 1 rounded up to 64; else 2 .. max_ctx + 1.  A
+                                sequence that needs more rows than this voids the results
+                                and the next call returns ECAPACITY.  Must be 0 in
+                                resident mode. */
 } asrkf_config;
 
 typedef struct {
@@ -86,6 +99,10 @@ typedef struct {
     int64_t attn_launches;      /* timed attention launches (asrkf_set_timing) */
     double  attn_kernel_ms;     /* summed duration of those launches */
     double  compression;        /* 1 - active_positions / total_positions */
+    int64_t rows_to_host;       /* spill mode: tokens whose K and V rows were copied to the
+                                   host store (each token at most once per layer) */
+    int64_t rows_from_host;     /* spill mode: token rows copied back to the device */
+    int64_t rows_released;      /* spill mode: device rows given up by freezing tokens */
 } asrkf_stats_t;
 
 typedef struct asrkf_ctx asrkf_ctx;
@@ -156,6 +173,18 @@ asrkf_status asrkf_set_timing(asrkf_ctx* ctx, int32_t enable);
 asrkf_status asrkf_get_state(asrkf_ctx* ctx, int32_t layer, int32_t seq,
                              int32_t* n_positions, int32_t* unfreeze_step, int32_t* count,
                              uint8_t* frozen, int32_t* active, int32_t* n_active);
+
+/* Where the K and V rows of one (layer, sequence) live after the last
+ * completed step (test export; Sec. 3.2 frozen storage).  Host outputs of at
+ * least max_ctx entries, any may be NULL:
+ *   n_positions: receives n_t
+ *   device_row:  [n_t] row of the device cache holding the position, or -1
+ *                when only the host store holds it (spill mode)
+ *   on_host:     [n_t] 1 if the host store holds the position's rows
+ * In resident mode device_row[p] = p and on_host is all 0.  Waits for all
+ * queued work of the context. */
+asrkf_status asrkf_get_residency(asrkf_ctx* ctx, int32_t layer, int32_t seq,
+                                 int32_t* n_positions, int32_t* device_row, uint8_t* on_host);
 
 /* Entropy monitor of one sequence after the last restore (Sec. 3.6):
  * entropy (nats), top probability, consecutive spike steps, level applied.

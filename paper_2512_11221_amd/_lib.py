@@ -29,6 +29,7 @@ class asrkf_config(ctypes.Structure):
         ("vocab", ctypes.c_int32), ("entropy_spike", ctypes.c_float),
         ("conf_drop", ctypes.c_float), ("wr_last_N", ctypes.c_int32),
         ("dtype", ctypes.c_int32), ("spill_min_D", ctypes.c_int32),
+        ("device_rows", ctypes.c_int32),
     ]
 
 
@@ -38,7 +39,8 @@ class asrkf_stats_t(ctypes.Structure):
         ("active_positions", ctypes.c_int64), ("attended_total", ctypes.c_int64),
         ("recoveries", ctypes.c_int64 * 4), ("rr_requests", ctypes.c_int64),
         ("attn_launches", ctypes.c_int64), ("attn_kernel_ms", ctypes.c_double),
-        ("compression", ctypes.c_double),
+        ("compression", ctypes.c_double), ("rows_to_host", ctypes.c_int64),
+        ("rows_from_host", ctypes.c_int64), ("rows_released", ctypes.c_int64),
     ]
 
     def as_dict(self):
@@ -75,6 +77,7 @@ def load():
         "asrkf_set_timing": ([P, I32], I32),
         "asrkf_get_state": ([P, I32, I32, P, P, P, P, P, P], I32),
         "asrkf_get_seq": ([P, I32, P, P, P, P], I32),
+        "asrkf_get_residency": ([P, I32, I32, P, P, P], I32),
         "asrkf_schedule_table": ([F, I32, P], I32),
         "asrkf_destroy": ([P], None),
         "asrkf_last_error": ([], ctypes.c_char_p),
@@ -115,10 +118,10 @@ def _stream(s):
 
 def make_config(n_layers, batch, n_q_heads, n_kv_heads, head_dim, max_ctx, window_K, tau,
                 k_soft, vocab, entropy_spike=math.inf, conf_drop=0.0, wr_last_N=0,
-                dtype="bf16", spill_min_D=0):
+                dtype="bf16", spill_min_D=0, device_rows=0):
     return asrkf_config(n_layers, batch, n_q_heads, n_kv_heads, head_dim, max_ctx, window_K,
                         tau, k_soft, vocab, entropy_spike, conf_drop, wr_last_N,
-                        BF16 if dtype == "bf16" else F32, spill_min_D)
+                        BF16 if dtype == "bf16" else F32, spill_min_D, device_rows)
 
 
 def asrkf_init(cfg):
@@ -169,6 +172,18 @@ def asrkf_get_state(ctx, layer, seq, max_ctx):
     k = n.value
     return {"n": k, "unfreeze": U[:k].copy(), "count": c[:k].copy(),
             "frozen": fr[:k].astype(bool), "active": act[: na.value].copy()}
+
+
+def asrkf_get_residency(ctx, layer, seq, max_ctx):
+    """Returns dict(n, device_row, on_host) as numpy arrays."""
+    import numpy as np
+    n = ctypes.c_int32()
+    row = np.zeros(max_ctx + 1, np.int32)
+    oh = np.zeros(max_ctx + 1, np.uint8)
+    _check(load().asrkf_get_residency(ctx, layer, seq, ctypes.addressof(n), row.ctypes.data,
+                                      oh.ctypes.data))
+    k = n.value
+    return {"n": k, "device_row": row[:k].copy(), "on_host": oh[:k].astype(bool)}
 
 
 def asrkf_get_seq(ctx, seq):

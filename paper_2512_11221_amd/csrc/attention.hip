@@ -188,8 +188,10 @@ attention_kernel(AttnArgs a) {
     int32_t* seq_off = lds;                                      // [B + 1]
     int32_t* dur_lds = lds + ((a.B + 1 + 3) & ~3);               // [kDurCache]
     int32_t* pos_lds = dur_lds + kDurCache;                      // [kChunk]
-    uint8_t* flag_lds = reinterpret_cast<uint8_t*>(pos_lds + kChunk);   // [kChunk]
-    float* merge_lds = reinterpret_cast<float*>(flag_lds + kChunk);    // [kWaves/2][NV][64]
+    int32_t* row_lds = pos_lds + kChunk;                         // [kChunk] (spill mode)
+    uint8_t* flag_lds = reinterpret_cast<uint8_t*>(row_lds + kChunk);   // [kChunk]
+    // the wave-state merge runs after the chunk loop: it reuses the chunk buffers
+    float* merge_lds = reinterpret_cast<float*>(pos_lds);        // [kWaves/2][NV][64]
 
     for (int i = threadIdx.x; i < kDurCache; i += blockDim.x) dur_lds[i] = a.dur[min(i, a.dur_len - 1)];
     plan_ranges(a.n_active, a.B, seq_off);
@@ -236,8 +238,10 @@ attention_kernel(AttnArgs a) {
         const int n_pos = a.plen[b] + a.t;       // positions after the append
         const int wedge = n_pos - a.window_K;    // positions < wedge are outside the window
         const size_t seq_row = (size_t)b * a.cap;
-        const size_t seg = seq_row * row_stride;
+        const size_t seg = (size_t)b * a.pool_rows * row_stride;
         const int32_t* list_b = a.list + seq_row;
+        const int32_t* lrow_b = a.list_row + seq_row;
+        const bool spill = a.spill != 0;
 
         uint4 qr[G][NC];
         {
@@ -256,7 +260,7 @@ attention_kernel(AttnArgs a) {
 #pragma unroll
             for (int e = 0; e < EL; ++e) st.acc[h][e] = 0.f;
         }
-        const int nbytes = a.cap * row_stride;
+        const int nbytes = a.pool_rows * row_stride;
         const __amdgpu_buffer_rsrc_t rk = __builtin_amdgcn_make_buffer_rsrc(
             (void*)((const char*)a.kpool + seg), (short)0, nbytes, kBufferFlags);
         const __amdgpu_buffer_rsrc_t rv = __builtin_amdgcn_make_buffer_rsrc(
@@ -266,7 +270,8 @@ attention_kernel(AttnArgs a) {
             const int len = min(kChunk, i1 - c0);
             if (c0 + len == nb) {
                 // this chunk ends with the new token: append its row to the cache first
-                const size_t dst = seg + (size_t)(n_pos - 1) * row_stride;
+                const int new_row = spill ? lrow_b[nb - 1] : n_pos - 1;
+                const size_t dst = seg + (size_t)new_row * row_stride;
                 const size_t src = (size_t)b * row_stride;
                 for (int o = threadIdx.x * 16; o < row_stride; o += blockDim.x * 16) {
                     *reinterpret_cast<uint4*>((char*)a.kpool_w + dst + o) =
@@ -277,6 +282,7 @@ attention_kernel(AttnArgs a) {
             }
             for (int i = threadIdx.x; i < len; i += blockDim.x) {
                 pos_lds[i] = list_b[c0 + i];
+                if (spill) row_lds[i] = lrow_b[c0 + i];
                 flag_lds[i] = 0;
             }
             __threadfence_block();
@@ -290,10 +296,12 @@ attention_kernel(AttnArgs a) {
                 for (int u = 0; u < kUnroll; ++u) {
                     const int idx = tb + u * TPI + tk;
                     valid[u] = idx < len;
-                    pos[u] = pos_lds[valid[u] ? idx : tb];
+                    const int li = valid[u] ? idx : tb;
+                    pos[u] = pos_lds[li];
+                    const int drow = spill ? row_lds[li] : pos[u];     // device row of the token
                     int vo = lane_off, so = 0;
-                    if constexpr (TPI == 1) so = wave_uniform(pos[u]) * row_stride;
-                    else vo += pos[u] * row_stride;
+                    if constexpr (TPI == 1) so = wave_uniform(drow) * row_stride;
+                    else vo += drow * row_stride;
 #pragma unroll
                     for (int c = 0; c < NC; ++c) {
                         kr[u][c] = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(rk, vo + c * 128, so, 0));
@@ -402,6 +410,7 @@ attention_kernel(AttnArgs a) {
                 fold<BF16, D, G>(st, bm, bl, bacc);
             }
         }
+        __syncthreads();                           // merge buffer reads done: chunks may restage
         if (wave == 0) {
             // merge the slots that hold the same KV head (different tokens of an iteration)
 #pragma unroll
@@ -526,8 +535,9 @@ constexpr int state_floats() { return 2 * G + G * Row<BF16, D>::kPerLane; }
 
 template <bool BF16, int D, int G>
 size_t lds_bytes(const AttnArgs& a) {
-    return (size_t)(((a.B + 1 + 3) & ~3) + kDurCache + kChunk) * 4 + kChunk +
-           (size_t)(kWaves / 2) * state_floats<BF16, D, G>() * 64 * 4;
+    const size_t chunk = (size_t)kChunk * (4 + 4 + 1);
+    const size_t merge = (size_t)(kWaves / 2) * state_floats<BF16, D, G>() * 64 * 4;
+    return (size_t)(((a.B + 1 + 3) & ~3) + kDurCache) * 4 + (chunk > merge ? chunk : merge);
 }
 
 // Timing events, when given, are recorded by the dispatch itself, so they

@@ -1,7 +1,7 @@
 // End-of-step rebuild of every active cache, with staged recovery fused in.
 //
 // One workgroup per (layer, sequence).  It streams the unfreeze steps U_p of
-// the n_t positions once and:
+// the n_t positions and:
 //   1. applies the recovery level chosen for the sequence (Sec. 3.6):
 //        SR: remaining timer U_p - (t+1) > 1     ->  U_p = t+1
 //        WR: p >= n_t - N and U_p > t+1          ->  U_p = t+1
@@ -12,6 +12,19 @@
 // A token frozen at step t' for d steps carries U = t' + d: stepping the
 // timers of Algorithm 1's second loop is the comparison against t+1, so the
 // per-step decrement pass over frozen storage disappears.
+//
+// Spill mode (Sec. 3.2: frozen KV leaves the GPU) adds device-row bookkeeping
+// to the same pass structure, all of it on the device:
+//   pass 1  a token frozen at step t for d >= spill_min_D steps gives its
+//           device row back to the sequence's free stack; if the host store
+//           does not hold its rows yet (K and V never change, so they are
+//           copied out once), the (position, row) pair goes to the out-list;
+//   pass 2  every position of the new active list that has no device row
+//           (its timer ran out, or recovery released it) takes one from the
+//           stack and goes to the in-list; the next token takes one too.
+// Rows are pushed and popped in ascending position order, so the assignment
+// is the same on every run.  The copies themselves are made by the transfer
+// kernel (out-list first, so a row is read before it is handed out again).
 //
 // The in-order compaction uses wave ballots: every thread owns 4 consecutive
 // positions (one 16-byte load), mbcnt over 4 ballots gives the exclusive
@@ -30,84 +43,281 @@ __device__ __forceinline__ int lanes_below(unsigned long long mask) {
                                      __builtin_amdgcn_mbcnt_lo((unsigned)mask, 0));
 }
 
+struct Ladder {
+    bool sr, wr, fr;
+    int t1, wr_from;
+};
+
+__device__ __forceinline__ Ladder make_ladder(const CompactArgs& a, int b, int n) {
+    const int level = a.forced_level >= 0 ? a.forced_level : (a.level ? a.level[b] : 0);
+    return Ladder{level == 1, level == 2, level == 3, a.t + 1, n - a.wr_last_N};
+}
+
+// Recovery select of one position.  Written with bitwise operators only: one
+// select per position, no short-circuit control flow.
+__device__ __forceinline__ int recover(const Ladder& r, int u, int q, bool live, bool& hit) {
+    const bool frozen_now = live & (u > r.t1);
+    hit = frozen_now & ((r.sr & (u > r.t1 + 1)) | (r.wr & (q >= r.wr_from)) | r.fr);
+    return hit ? r.t1 : u;
+}
+
+__device__ __forceinline__ void load4(const int32_t* src, int p, int n, int (&v)[4], int fill) {
+    if (p + 3 < n) {
+        const int4 x = *reinterpret_cast<const int4*>(src + p);
+        v[0] = x.x; v[1] = x.y; v[2] = x.z; v[3] = x.w;
+    } else {
+#pragma unroll
+        for (int k = 0; k < 4; ++k) v[k] = (p + k < n) ? src[p + k] : fill;
+    }
+}
+
+// Exclusive offsets inside the tile of up to two per-thread item counts, and
+// the tile totals.  Every thread of the block must call it.
+struct Scan {
+    int off0, off1, tot0, tot1;
+};
+
+__device__ __forceinline__ Scan tile_scan(int before0, int mine0, int before1, int mine1,
+                                          int* tot0, int* tot1) {
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    if (lane == 63) {
+        tot0[wave] = before0 + mine0;
+        tot1[wave] = before1 + mine1;
+    }
+    __syncthreads();
+    Scan s{before0, before1, 0, 0};
+    for (int w = 0; w < kWaves; ++w) {
+        const int c0 = tot0[w], c1 = tot1[w];
+        s.off0 += (w < wave) ? c0 : 0;
+        s.off1 += (w < wave) ? c1 : 0;
+        s.tot0 += c0;
+        s.tot1 += c1;
+    }
+    __syncthreads();                          // tot0/tot1 are rewritten by the next tile
+    return s;
+}
+
+// Ballot prefix of 4 per-position flags: items of lower lanes, own items.
+__device__ __forceinline__ void ballot4(const bool (&f)[4], int& before, int& mine) {
+    before = 0;
+    mine = 0;
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+        before += lanes_below(__ballot(f[k]));
+        mine += f[k];
+    }
+}
+
 __global__ void __launch_bounds__(kThreads)
 compact_kernel(CompactArgs a) {
-    __shared__ int wave_tot[kWaves];
-    __shared__ int tile_base;
+    __shared__ int tot0[kWaves], tot1[kWaves];
 
     const int inst = blockIdx.x;
     const int b = inst % a.B;
     const int n = a.plen[b] + a.t;            // positions after step t
-    const int t1 = a.t + 1;
-    const int level = a.forced_level >= 0 ? a.forced_level : (a.level ? a.level[b] : 0);
+    const Ladder r = make_ladder(a, b, n);
     int32_t* U = a.unfreeze + (size_t)inst * a.cap;
     int32_t* list = a.list + (size_t)inst * a.cap;
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int wr_from = n - a.wr_last_N;
-    const bool sr = level == 1, wr = level == 2, fr = level == 3;
-
-    if (tid == 0) tile_base = 0;
-    __syncthreads();
+    const int tid = threadIdx.x;
+    int listed = 0;
 
     for (int p0 = 0; p0 < n; p0 += 4 * kThreads) {
         const int p = p0 + 4 * tid;
-        int u[4] = {0, 0, 0, 0};
-        if (p + 3 < n) {
-            const int4 v = *reinterpret_cast<const int4*>(U + p);
-            u[0] = v.x; u[1] = v.y; u[2] = v.z; u[3] = v.w;
-        } else {
-            for (int k = 0; k < 4; ++k) if (p + k < n) u[k] = U[p + k];
-        }
-        // branch-free: one select per position, no short-circuit control flow
+        int u[4];
+        load4(U, p, n, u, 0);
         bool flag[4];
         bool dirty = false;
 #pragma unroll
         for (int k = 0; k < 4; ++k) {
-            const int q = p + k;
-            const bool live = q < n;
-            const bool frozen_now = live & (u[k] > t1);
-            const bool hit = frozen_now & ((sr & (u[k] > t1 + 1)) | (wr & (q >= wr_from)) | fr);
-            u[k] = hit ? t1 : u[k];
+            bool hit;
+            const bool live = p + k < n;
+            u[k] = recover(r, u[k], p + k, live, hit);
             dirty |= hit;
-            flag[k] = live & (u[k] <= t1);
+            flag[k] = live & (u[k] <= r.t1);
         }
         if (dirty) {
             for (int k = 0; k < 4; ++k) if (p + k < n) U[p + k] = u[k];
         }
-        unsigned long long bal[4];
-        int before = 0, mine = 0;
-#pragma unroll
-        for (int k = 0; k < 4; ++k) {
-            bal[k] = __ballot(flag[k]);
-            before += lanes_below(bal[k]);
-            mine += flag[k];
-        }
-        if (lane == 63) wave_tot[wave] = before + mine;
-        __syncthreads();
-        int wave_off = 0, tile_tot = 0;
-        for (int w = 0; w < kWaves; ++w) {
-            const int c = wave_tot[w];
-            wave_off += (w < wave) ? c : 0;
-            tile_tot += c;
-        }
-        int out = tile_base + wave_off + before;
+        int before, mine;
+        ballot4(flag, before, mine);
+        const Scan sc = tile_scan(before, mine, 0, 0, tot0, tot1);
+        int out = listed + sc.off0;
 #pragma unroll
         for (int k = 0; k < 4; ++k) if (flag[k]) list[out++] = p + k;
-        __syncthreads();
-        if (tid == 0) tile_base += tile_tot;
-        __syncthreads();
+        listed += sc.tot0;
     }
     if (tid == 0) {
-        list[tile_base] = n;                  // the next token's position
-        a.n_active[inst] = tile_base + 1;
-        atomicAdd(a.listed_total, (unsigned long long)(tile_base + 1));
+        list[listed] = n;                     // the next token's position
+        a.n_active[inst] = listed + 1;
+        atomicAdd(a.listed_total, (unsigned long long)(listed + 1));
     }
+}
+
+__global__ void __launch_bounds__(kThreads)
+compact_spill_kernel(CompactArgs a) {
+    __shared__ int tot0[kWaves], tot1[kWaves];
+
+    const int inst = blockIdx.x;
+    const int b = inst % a.B;
+    const int n = a.plen[b] + a.t;
+    const Ladder r = make_ladder(a, b, n);
+    const size_t base = (size_t)inst * a.cap;
+    int32_t* U = a.unfreeze + base;
+    int32_t* list = a.list + base;
+    int32_t* lrow = a.list_row + base;
+    int32_t* row_of = a.row_of + base;
+    uint8_t* on_host = a.on_host + base;
+    int32_t* stack = a.free_rows + (size_t)inst * a.pool_rows;
+    int32_t* out_pos = a.out_pos + base;
+    int32_t* out_row = a.out_row + base;
+    int32_t* in_pos = a.in_pos + base;
+    int32_t* in_row = a.in_row + base;
+    const int tid = threadIdx.x;
+    const int top0 = a.free_top[inst];
+
+    // pass 1: recovery, then release the rows of tokens frozen now for d >= spill_min_D
+    int pushed = 0, n_out = 0;
+    for (int p0 = 0; p0 < n; p0 += 4 * kThreads) {
+        const int p = p0 + 4 * tid;
+        int u[4], row[4];
+        load4(U, p, n, u, 0);
+        load4(row_of, p, n, row, -1);
+        bool spill[4], first[4];
+        bool dirty = false;
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+            bool hit;
+            const bool live = p + k < n;
+            u[k] = recover(r, u[k], p + k, live, hit);
+            dirty |= hit;
+            // frozen at step t (U = t + d) for d >= spill_min_D, and still in a device row
+            spill[k] = live & (row[k] >= 0) & (u[k] > r.t1) & (u[k] - a.t >= a.spill_min_D);
+            const bool stored = live ? on_host[p + k] != 0 : true;
+            first[k] = spill[k] & !stored;
+        }
+        if (dirty) {
+            for (int k = 0; k < 4; ++k) if (p + k < n) U[p + k] = u[k];
+        }
+        int b0, m0, b1, m1;
+        ballot4(spill, b0, m0);
+        ballot4(first, b1, m1);
+        const Scan sc = tile_scan(b0, m0, b1, m1, tot0, tot1);
+        int ps = top0 + pushed + sc.off0, po = n_out + sc.off1;
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+            if (first[k]) {
+                out_pos[po] = p + k;
+                out_row[po] = row[k];
+                on_host[p + k] = 1;
+                ++po;
+            }
+            if (spill[k]) {
+                if (ps < a.pool_rows) stack[ps] = row[k];
+                row_of[p + k] = -1;
+                ++ps;
+            }
+        }
+        pushed += sc.tot0;
+        n_out += sc.tot1;
+    }
+    __syncthreads();                          // stack and row_of writes are read below
+    const int top = min(a.pool_rows, top0 + pushed);
+
+    // pass 2: the active list of step t+1, device rows for positions that lack one
+    int listed = 0, popped = 0;
+    bool short_of_rows = false;
+    for (int p0 = 0; p0 < n; p0 += 4 * kThreads) {
+        const int p = p0 + 4 * tid;
+        int u[4], row[4];
+        load4(U, p, n, u, 0);
+        load4(row_of, p, n, row, -1);
+        bool flag[4], need[4];
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+            flag[k] = (p + k < n) & (u[k] <= r.t1);
+            need[k] = flag[k] & (row[k] < 0);
+        }
+        int b0, m0, b1, m1;
+        ballot4(flag, b0, m0);
+        ballot4(need, b1, m1);
+        const Scan sc = tile_scan(b0, m0, b1, m1, tot0, tot1);
+        int pl = listed + sc.off0, pn = popped + sc.off1;
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+            if (!flag[k]) continue;
+            int dev = row[k];
+            if (need[k]) {
+                const int idx = top - 1 - pn;
+                if (idx >= 0) {
+                    dev = stack[idx];
+                    row_of[p + k] = dev;
+                    in_pos[pn] = p + k;
+                    in_row[pn] = dev;
+                } else {
+                    dev = 0;                  // no row left: results are void, the host is told
+                    short_of_rows = true;
+                }
+                ++pn;
+            }
+            list[pl] = p + k;
+            lrow[pl] = dev;
+            ++pl;
+        }
+        listed += sc.tot0;
+        popped += sc.tot1;
+    }
+    if (short_of_rows) *a.overflow = 1;
+    __syncthreads();
+    if (tid == 0) {
+        const int restored = min(popped, top);
+        const int idx = top - 1 - popped;     // the next token's row
+        int dev = 0;
+        if (idx >= 0) {
+            dev = stack[idx];
+            row_of[n] = dev;
+        } else {
+            *a.overflow = 1;
+        }
+        list[listed] = n;
+        lrow[listed] = dev;
+        a.free_top[inst] = max(0, idx);
+        a.n_out[inst] = n_out;
+        a.n_in[inst] = restored;
+        a.n_active[inst] = listed + 1;
+        atomicAdd(a.listed_total, (unsigned long long)(listed + 1));
+        if (n_out) atomicAdd(a.xfer + 0, (unsigned long long)n_out);
+        if (restored) atomicAdd(a.xfer + 1, (unsigned long long)restored);
+        if (pushed) atomicAdd(a.xfer + 2, (unsigned long long)pushed);
+    }
+}
+
+__global__ void __launch_bounds__(256)
+spill_init_kernel(SpillInitArgs a) {
+    const int inst = blockIdx.x;
+    const int P = a.plen[inst % a.B];
+    const size_t base = (size_t)inst * a.cap;
+    for (int p = threadIdx.x; p < a.cap; p += blockDim.x) {
+        a.row_of[base + p] = p < P ? p : -1;
+        a.on_host[base + p] = 0;
+    }
+    const int free_n = max(0, a.pool_rows - P);
+    int32_t* stack = a.free_rows + (size_t)inst * a.pool_rows;
+    for (int k = threadIdx.x; k < free_n; k += blockDim.x) stack[k] = a.pool_rows - 1 - k;
+    if (threadIdx.x == 0) a.free_top[inst] = free_n;
 }
 
 }  // namespace
 
 hipError_t launch_compact(const CompactArgs& a, int n_instances, hipStream_t s) {
-    hipLaunchKernelGGL(compact_kernel, dim3(n_instances), dim3(kThreads), 0, s, a);
+    if (a.spill_min_D > 0)
+        hipLaunchKernelGGL(compact_spill_kernel, dim3(n_instances), dim3(kThreads), 0, s, a);
+    else
+        hipLaunchKernelGGL(compact_kernel, dim3(n_instances), dim3(kThreads), 0, s, a);
+    return hipGetLastError();
+}
+
+hipError_t launch_spill_init(const SpillInitArgs& a, int n_instances, hipStream_t s) {
+    hipLaunchKernelGGL(spill_init_kernel, dim3(n_instances), dim3(256), 0, s, a);
     return hipGetLastError();
 }
 

@@ -15,7 +15,7 @@ namespace asrkf {
 constexpr int kMaxBatch = 1024;
 
 struct AttnArgs {
-    const void* kpool;        // layer base, [B][cap][Hkv][D]
+    const void* kpool;        // layer base, [B][pool_rows][Hkv][D]
     const void* vpool;
     const void* q;            // [B][Hq][D]
     const void* knew;         // [B][Hkv][D]
@@ -23,6 +23,8 @@ struct AttnArgs {
     void* kpool_w;            // same as kpool, writable (append)
     void* vpool_w;
     const int32_t* list;      // layer base, [B][cap] ascending positions
+    const int32_t* list_row;  // layer base, [B][cap] device row of each listed position
+                              // (spill mode only; in resident mode the row is the position)
     const int32_t* n_active;  // layer base, [B]
     const int32_t* plen;      // [B] prompt length
     int32_t* unfreeze;        // layer base, [B][cap]: U_j
@@ -33,6 +35,8 @@ struct AttnArgs {
     int32_t* slot_first;      // [B] first partial slot of each sequence (written)
     int32_t* slot_end;        // [B] one past its last slot (written)
     int32_t B, cap, Hq, Hkv;
+    int32_t pool_rows;        // device rows per sequence (cap in resident mode)
+    int32_t spill;            // 1: rows come from list_row
     int32_t t;                // current step (1-based)
     int32_t window_K;
     int32_t dur_len;
@@ -60,6 +64,47 @@ struct CompactArgs {
     int32_t forced_level;     // -1: read level[]; 0: none; 1..3 forced SR/WR/FR
     int32_t t;                // completed step; lists are built for step t+1
     int32_t B, cap, wr_last_N;
+    // spill mode only (spill_min_D > 0)
+    int32_t spill_min_D;
+    int32_t pool_rows;        // device rows per (layer, sequence)
+    int32_t* row_of;          // [L][B][cap] device row of a position, -1: host store only
+    uint8_t* on_host;         // [L][B][cap] 1: the host store holds the position's rows
+    int32_t* list_row;        // [L][B][cap] device row of each listed position
+    int32_t* free_rows;       // [L][B][pool_rows] stack of free device rows
+    int32_t* free_top;        // [L][B] stack height
+    int32_t* out_pos;         // [L][B][cap] rows to copy to the host store: position ...
+    int32_t* out_row;         //   ... and the device row it leaves
+    int32_t* n_out;           // [L][B]
+    int32_t* in_pos;          // [L][B][cap] rows to copy back: position ...
+    int32_t* in_row;          //   ... and the device row it takes
+    int32_t* n_in;            // [L][B]
+    int32_t* overflow;        // set to 1 when a sequence needs more device rows than it has
+    unsigned long long* xfer; // [0] rows to host, [1] rows from host, [2] device rows released
+};
+
+// First decode step in spill mode: prompt positions p < P sit in device rows
+// p, the other rows are free (lowest handed out first), nothing is on the host.
+struct SpillInitArgs {
+    int32_t* row_of;
+    uint8_t* on_host;
+    int32_t* free_rows;
+    int32_t* free_top;
+    const int32_t* plen;
+    int32_t B, cap, pool_rows;
+};
+
+// Row copies between the device cache and the host store (spill mode).
+struct XferArgs {
+    char* kpool;              // [L][B][pool_rows][row_bytes]
+    char* vpool;
+    char* khost;              // device-visible pointer of the pinned store, [L][B][cap][row_bytes]
+    char* vhost;
+    const int32_t* pos;       // [L][B][cap] per-instance lists of positions ...
+    const int32_t* row;       //   ... and device rows
+    const int32_t* count;     // [L][B] list lengths
+    int32_t inst0;            // first (layer, sequence) instance of the launch
+    int32_t cap, pool_rows, row_bytes;
+    int32_t to_host;          // 1: device -> host store, 0: host store -> device
 };
 
 constexpr int kEntropySplit = 32;   // workgroups per sequence in the entropy pass
@@ -86,6 +131,8 @@ hipError_t attention_occupancy(const AttnArgs& a, int dtype_bf16, int head_dim, 
                                int* blocks_per_cu);
 hipError_t launch_finish(const FinishArgs& a, int head_dim, hipStream_t s);
 hipError_t launch_compact(const CompactArgs& a, int n_instances, hipStream_t s);
+hipError_t launch_spill_init(const SpillInitArgs& a, int n_instances, hipStream_t s);
+hipError_t launch_xfer(const XferArgs& a, int n_instances, hipStream_t s);
 hipError_t launch_entropy(const EntropyArgs& a, hipStream_t s);
 
 }  // namespace asrkf

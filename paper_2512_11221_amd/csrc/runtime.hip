@@ -1,7 +1,8 @@
 // Context, memory layout and the C ABI declared in include/asrkf.h.
 //
-// HBM layout of a context (cap = max_ctx + 1 rounded up to 64 positions):
-//   K, V cache      [L][B][cap][Hkv][D]   dtype   token-major rows
+// HBM layout of a context (cap = max_ctx + 1 rounded up to 64 positions;
+// pool_rows = cap in resident mode, the configured device rows in spill mode):
+//   K, V cache      [L][B][pool_rows][Hkv][D]   dtype   token-major rows
 //   unfreeze U      [L][B][cap]           int32   token attends at step t iff U <= t
 //   count c         [L][B][cap]           int32   low-relevance detections (Eq. 3)
 //   active list     [L][B][cap]           int32   ascending positions for the step
@@ -9,6 +10,10 @@
 //   partials        [grid+B][Hq][D+2]     fp32    split-K attention partials
 //   per sequence    prompt length, escalation, level, entropy, p_max
 //   duration table  [max_ctx + 2]         int32   d(c) of Eq. 3, built exactly on the host
+// Spill mode adds, per (layer, sequence): the device row of every position,
+// a host-store flag, the device row of every listed position, a stack of
+// free rows and the out/in copy lists; and a pinned host store
+// [L][B][cap][Hkv][D] for K and V, written once per token.
 #include <math.h>
 #include <stdarg.h>
 #include <stdio.h>
@@ -27,6 +32,8 @@ using namespace asrkf;
 namespace {
 
 thread_local std::string g_last_error;
+
+constexpr int kCounters = 16;   // device counters of a context (see asrkf_ctx::counters)
 
 asrkf_status fail(asrkf_status st, const char* fmt, ...) {
     char buf[512];
@@ -95,7 +102,35 @@ struct asrkf_ctx {
     int32_t* slot_info = nullptr;   // [2B]: first slot, end slot per sequence
     float* ent_partial = nullptr;   // [B][kEntropySplit][3]
     int32_t* ent_ticket = nullptr;  // [B]
-    unsigned long long* counters = nullptr;   // [0] listed_total, [1..3] recoveries, [5] rr
+    unsigned long long* counters = nullptr;   // [0] listed_total, [1..3] recoveries, [5] rr,
+                                              // [8] rows to host, [9] rows from host, [10] released
+
+    // spill mode
+    bool spill = false;
+    int pool_rows = 0;            // device rows per (layer, seq)
+    int32_t* row_of = nullptr;
+    uint8_t* on_host = nullptr;
+    int32_t* list_row = nullptr;
+    int32_t* free_rows = nullptr;
+    int32_t* free_top = nullptr;
+    int32_t* out_pos = nullptr;
+    int32_t* out_row = nullptr;
+    int32_t* n_out = nullptr;
+    int32_t* in_pos = nullptr;
+    int32_t* in_row = nullptr;
+    int32_t* n_in = nullptr;
+    int32_t* overflow = nullptr;
+    void* khost = nullptr;        // pinned host store (host pointers)
+    void* vhost = nullptr;
+    void* khost_dev = nullptr;    // the same memory as seen by kernels
+    void* vhost_dev = nullptr;
+    int32_t* overflow_host = nullptr;   // pinned copy of *overflow
+    hipStream_t side = nullptr;   // copies to and from the host store
+    hipEvent_t ev_lists = nullptr;      // compaction done (main stream)
+    hipEvent_t ev_flag = nullptr;       // overflow flag copied to the host
+    std::vector<hipEvent_t> ev_in;      // per layer: its restores are in the device cache
+    bool xfer_recorded = false;
+    bool flag_recorded = false;
 
     std::vector<int32_t> plen_host;
     std::vector<char> prefilled;   // per sequence
@@ -148,8 +183,16 @@ void free_all(asrkf_ctx* ctx) {
     void* ptrs[] = {ctx->kpool, ctx->vpool, ctx->unfreeze, ctx->count, ctx->list,
                     ctx->n_active, ctx->plen, ctx->dur, ctx->escalation, ctx->level,
                     ctx->entropy, ctx->pmax, ctx->part_acc, ctx->part_ml, ctx->slot_info, ctx->ent_partial, ctx->ent_ticket,
-                    ctx->counters};
+                    ctx->counters, ctx->row_of, ctx->on_host, ctx->list_row, ctx->free_rows,
+                    ctx->free_top, ctx->out_pos, ctx->out_row, ctx->n_out, ctx->in_pos, ctx->in_row,
+                    ctx->n_in, ctx->overflow};
     for (void* p : ptrs) if (p) (void)hipFree(p);
+    void* host[] = {ctx->khost, ctx->vhost, ctx->overflow_host};
+    for (void* p : host) if (p) (void)hipHostFree(p);
+    if (ctx->side) (void)hipStreamDestroy(ctx->side);
+    if (ctx->ev_lists) (void)hipEventDestroy(ctx->ev_lists);
+    if (ctx->ev_flag) (void)hipEventDestroy(ctx->ev_flag);
+    for (hipEvent_t e : ctx->ev_in) if (e) (void)hipEventDestroy(e);
     for (auto& ev : ctx->ev_used) { (void)hipEventDestroy(ev.first); (void)hipEventDestroy(ev.second); }
     for (auto& ev : ctx->ev_free) { (void)hipEventDestroy(ev.first); (void)hipEventDestroy(ev.second); }
 }
@@ -172,7 +215,11 @@ asrkf_status validate(const asrkf_config* c) {
     if (c->vocab < 1) return fail(ASRKF_EINVAL, "vocab must be >= 1");
     if (isnan(c->entropy_spike) || isnan(c->conf_drop)) return fail(ASRKF_EINVAL, "NaN threshold");
     if (c->dtype != ASRKF_BF16 && c->dtype != ASRKF_F32) return fail(ASRKF_EINVAL, "unknown dtype");
-    if (c->spill_min_D != 0) return fail(ASRKF_EINVAL, "spill mode is not available in this build");
+    if (c->spill_min_D < 0) return fail(ASRKF_EINVAL, "spill_min_D must be >= 0");
+    if (c->spill_min_D == 0 && c->device_rows != 0)
+        return fail(ASRKF_EINVAL, "device_rows applies to spill mode only (spill_min_D > 0)");
+    if (c->device_rows != 0 && (c->device_rows < 2 || c->device_rows > c->max_ctx + 1))
+        return fail(ASRKF_EINVAL, "device_rows must be 0 or in 2..max_ctx+1");
     {
         const int64_t row = (int64_t)c->n_kv_heads * c->head_dim * (c->dtype == ASRKF_BF16 ? 2 : 4);
         const int64_t cap = ((int64_t)c->max_ctx + 1 + 63) / 64 * 64;
@@ -235,6 +282,8 @@ asrkf_status asrkf_init(const asrkf_config* cfg, asrkf_ctx** out) {
     }
     ctx->n_slots = ctx->grid + c.batch;
     ctx->dur_len = c.max_ctx + 2;
+    ctx->spill = c.spill_min_D > 0;
+    ctx->pool_rows = ctx->spill && c.device_rows > 0 ? c.device_rows : ctx->cap;
 
     const size_t inst = (size_t)c.n_layers * c.batch;
     const size_t per_pos = inst * ctx->cap;
@@ -243,8 +292,9 @@ asrkf_status asrkf_init(const asrkf_config* cfg, asrkf_ctx** out) {
         st = dev_alloc(ctx, &ctx->field, (bytes));                \
         if (st != ASRKF_OK) { free_all(ctx); delete ctx; return st; } \
     } while (0)
-    ALLOC(kpool, per_pos * ctx->row_bytes);
-    ALLOC(vpool, per_pos * ctx->row_bytes);
+    const size_t pool_bytes = inst * ctx->pool_rows * ctx->row_bytes;
+    ALLOC(kpool, pool_bytes);
+    ALLOC(vpool, pool_bytes);
     ALLOC(unfreeze, per_pos * 4);
     ALLOC(count, per_pos * 4);
     ALLOC(list, per_pos * 4);
@@ -260,7 +310,48 @@ asrkf_status asrkf_init(const asrkf_config* cfg, asrkf_ctx** out) {
     ALLOC(slot_info, (size_t)c.batch * 2 * 4);
     ALLOC(ent_partial, (size_t)c.batch * kEntropySplit * 3 * 4);
     ALLOC(ent_ticket, (size_t)c.batch * 4);
-    ALLOC(counters, 8 * sizeof(unsigned long long));
+    ALLOC(counters, kCounters * sizeof(unsigned long long));
+    if (ctx->spill) {
+        ALLOC(row_of, per_pos * 4);
+        ALLOC(on_host, per_pos);
+        ALLOC(list_row, per_pos * 4);
+        ALLOC(free_rows, inst * ctx->pool_rows * 4);
+        ALLOC(free_top, inst * 4);
+        ALLOC(out_pos, per_pos * 4);
+        ALLOC(out_row, per_pos * 4);
+        ALLOC(n_out, inst * 4);
+        ALLOC(in_pos, per_pos * 4);
+        ALLOC(in_row, per_pos * 4);
+        ALLOC(n_in, inst * 4);
+        ALLOC(overflow, 4);
+        // host store: pinned, mapped, coarse-grained (only the GPU reads and writes it)
+        const size_t store = per_pos * ctx->row_bytes;
+        const unsigned flags = hipHostMallocMapped | hipHostMallocNonCoherent;
+        hipError_t he = hipHostMalloc(&ctx->khost, store, flags);
+        if (he == hipSuccess) he = hipHostMalloc(&ctx->vhost, store, flags);
+        if (he == hipSuccess) he = hipHostMalloc((void**)&ctx->overflow_host, 64, hipHostMallocDefault);
+        if (he != hipSuccess) {
+            (void)hipGetLastError();
+            free_all(ctx);
+            delete ctx;
+            return fail(ASRKF_ENOMEM, "pinned host store of 2 x %zu bytes: %s", store, hipGetErrorString(he));
+        }
+        *ctx->overflow_host = 0;
+        he = hipHostGetDevicePointer(&ctx->khost_dev, ctx->khost, 0);
+        if (he == hipSuccess) he = hipHostGetDevicePointer(&ctx->vhost_dev, ctx->vhost, 0);
+        if (he == hipSuccess) he = hipStreamCreateWithFlags(&ctx->side, hipStreamNonBlocking);
+        if (he == hipSuccess) he = hipEventCreateWithFlags(&ctx->ev_lists, hipEventDisableTiming);
+        if (he == hipSuccess) he = hipEventCreateWithFlags(&ctx->ev_flag, hipEventDisableTiming);
+        ctx->ev_in.assign(c.n_layers, nullptr);
+        for (int l = 0; l < c.n_layers && he == hipSuccess; ++l)
+            he = hipEventCreateWithFlags(&ctx->ev_in[l], hipEventDisableTiming);
+        if (he != hipSuccess) {
+            st = hip_fail(nullptr, he, "spill-mode stream, events or mapping");
+            free_all(ctx);
+            delete ctx;
+            return st;
+        }
+    }
 #undef ALLOC
 
     std::vector<int32_t> table(ctx->dur_len);
@@ -279,7 +370,8 @@ asrkf_status asrkf_init(const asrkf_config* cfg, asrkf_ctx** out) {
     INIT(hipMemset(ctx->entropy, 0, (size_t)c.batch * 4));
     INIT(hipMemset(ctx->pmax, 0, (size_t)c.batch * 4));
     INIT(hipMemset(ctx->ent_ticket, 0, (size_t)c.batch * 4));
-    INIT(hipMemset(ctx->counters, 0, 8 * sizeof(unsigned long long)));
+    INIT(hipMemset(ctx->counters, 0, kCounters * sizeof(unsigned long long)));
+    if (ctx->spill) INIT(hipMemset(ctx->overflow, 0, 4));
     INIT(hipMemcpy(ctx->dur, table.data(), table.size() * 4, hipMemcpyHostToDevice));
     INIT(hipDeviceSynchronize());
 #undef INIT
@@ -298,12 +390,15 @@ asrkf_status asrkf_prefill(asrkf_ctx* ctx, int32_t layer, int32_t seq, const voi
         return fail(ASRKF_EINVAL, "layer or sequence out of range");
     if (n_tokens < 1 || n_tokens > c.max_ctx - 1)
         return fail(ASRKF_EINVAL, "n_tokens must be in 1..max_ctx-1");
+    if (n_tokens > ctx->pool_rows - 1)
+        return fail(ASRKF_EINVAL, "n_tokens must leave one device row free (device_rows = %d)",
+                    ctx->pool_rows);
     if (!k || !v) return fail(ASRKF_EINVAL, "null k or v");
     if (ctx->prefilled[seq] && ctx->plen_host[seq] != n_tokens)
         return fail(ASRKF_EINVAL, "sequence %d was prefilled with %d tokens in another layer",
                     seq, ctx->plen_host[seq]);
     hipStream_t s = static_cast<hipStream_t>(stream);
-    const size_t off = ((size_t)layer * c.batch + seq) * ctx->cap * ctx->row_bytes;
+    const size_t off = ((size_t)layer * c.batch + seq) * ctx->pool_rows * ctx->row_bytes;
     const size_t bytes = (size_t)n_tokens * ctx->row_bytes;
     HIP_OK(ctx, hipMemcpyAsync((char*)ctx->kpool + off, k, bytes, hipMemcpyDeviceToDevice, s));
     HIP_OK(ctx, hipMemcpyAsync((char*)ctx->vpool + off, v, bytes, hipMemcpyDeviceToDevice, s));
@@ -320,6 +415,19 @@ asrkf_status asrkf_prefill(asrkf_ctx* ctx, int32_t layer, int32_t seq, const voi
 namespace {
 
 asrkf_status build_lists(asrkf_ctx* ctx, int forced_level, hipStream_t s) {
+    const int n_inst = ctx->cfg.n_layers * ctx->cfg.batch;
+    if (ctx->spill && ctx->t == 0) {
+        SpillInitArgs z{};
+        z.row_of = ctx->row_of;
+        z.on_host = ctx->on_host;
+        z.free_rows = ctx->free_rows;
+        z.free_top = ctx->free_top;
+        z.plen = ctx->plen;
+        z.B = ctx->cfg.batch;
+        z.cap = ctx->cap;
+        z.pool_rows = ctx->pool_rows;
+        HIP_OK(ctx, launch_spill_init(z, n_inst, s));
+    }
     CompactArgs a{};
     a.unfreeze = ctx->unfreeze;
     a.list = ctx->list;
@@ -332,7 +440,78 @@ asrkf_status build_lists(asrkf_ctx* ctx, int forced_level, hipStream_t s) {
     a.B = ctx->cfg.batch;
     a.cap = ctx->cap;
     a.wr_last_N = ctx->cfg.wr_last_N;
-    HIP_OK(ctx, launch_compact(a, ctx->cfg.n_layers * ctx->cfg.batch, s));
+    if (ctx->spill) {
+        a.spill_min_D = ctx->cfg.spill_min_D;
+        a.pool_rows = ctx->pool_rows;
+        a.row_of = ctx->row_of;
+        a.on_host = ctx->on_host;
+        a.list_row = ctx->list_row;
+        a.free_rows = ctx->free_rows;
+        a.free_top = ctx->free_top;
+        a.out_pos = ctx->out_pos;
+        a.out_row = ctx->out_row;
+        a.n_out = ctx->n_out;
+        a.in_pos = ctx->in_pos;
+        a.in_row = ctx->in_row;
+        a.n_in = ctx->n_in;
+        a.overflow = ctx->overflow;
+        a.xfer = ctx->counters + 8;
+    }
+    HIP_OK(ctx, launch_compact(a, n_inst, s));
+    if (!ctx->spill) return ASRKF_OK;
+
+    // the flag tells the host (one step late, without a wait) that rows ran out
+    HIP_OK(ctx, hipMemcpyAsync(ctx->overflow_host, ctx->overflow, 4, hipMemcpyDeviceToHost, s));
+    HIP_OK(ctx, hipEventRecord(ctx->ev_flag, s));
+    ctx->flag_recorded = true;
+
+    // copies on the side stream: every out-list first (its rows may be handed
+    // out again below), then each layer's in-list, which that layer's next
+    // attention launch waits for
+    HIP_OK(ctx, hipEventRecord(ctx->ev_lists, s));
+    HIP_OK(ctx, hipStreamWaitEvent(ctx->side, ctx->ev_lists, 0));
+    XferArgs x{};
+    x.kpool = static_cast<char*>(ctx->kpool);
+    x.vpool = static_cast<char*>(ctx->vpool);
+    x.khost = static_cast<char*>(ctx->khost_dev);
+    x.vhost = static_cast<char*>(ctx->vhost_dev);
+    x.cap = ctx->cap;
+    x.pool_rows = ctx->pool_rows;
+    x.row_bytes = (int32_t)ctx->row_bytes;
+    x.pos = ctx->out_pos;
+    x.row = ctx->out_row;
+    x.count = ctx->n_out;
+    x.inst0 = 0;
+    x.to_host = 1;
+    HIP_OK(ctx, launch_xfer(x, n_inst, ctx->side));
+    x.pos = ctx->in_pos;
+    x.row = ctx->in_row;
+    x.count = ctx->n_in;
+    x.to_host = 0;
+    for (int l = 0; l < ctx->cfg.n_layers; ++l) {
+        x.inst0 = l * ctx->cfg.batch;
+        HIP_OK(ctx, launch_xfer(x, ctx->cfg.batch, ctx->side));
+        HIP_OK(ctx, hipEventRecord(ctx->ev_in[l], ctx->side));
+    }
+    ctx->xfer_recorded = true;
+    return ASRKF_OK;
+}
+
+// Spill mode: a sequence ran out of device rows at an earlier step.  Checked
+// without waiting (the flag copy of the last rebuild may still be queued) or,
+// from the synchronizing calls, after a full wait.
+asrkf_status check_overflow(asrkf_ctx* ctx, bool synced) {
+    if (!ctx->spill || !ctx->flag_recorded) return ASRKF_OK;
+    if (!synced) {
+        const hipError_t q = hipEventQuery(ctx->ev_flag);
+        if (q == hipErrorNotReady) return ASRKF_OK;
+        if (q != hipSuccess) return hip_fail(ctx, q, "hipEventQuery");
+    }
+    if (*(volatile int32_t*)ctx->overflow_host) {
+        ctx->poisoned = true;
+        return fail(ASRKF_ECAPACITY, "a sequence needed more than device_rows = %d device rows; "
+                    "results since then are void", ctx->pool_rows);
+    }
     return ASRKF_OK;
 }
 
@@ -352,16 +531,24 @@ asrkf_status asrkf_decode_step(asrkf_ctx* ctx, int32_t layer, const void* q, con
     for (int b = 0; b < c.batch; ++b)
         if (ctx->plen_host[b] + t > c.max_ctx)
             return fail(ASRKF_ECAPACITY, "sequence %d would exceed max_ctx=%d", b, c.max_ctx);
+    st = check_overflow(ctx, false);
+    if (st != ASRKF_OK) return st;
     hipStream_t s = static_cast<hipStream_t>(stream);
     if (!ctx->lists_ready) {
+        if (ctx->spill)
+            for (int b = 0; b < c.batch; ++b)
+                if (ctx->plen_host[b] + 1 > ctx->pool_rows)
+                    return fail(ASRKF_ECAPACITY, "sequence %d: prompt leaves no free device row", b);
         st = build_lists(ctx, 0, s);          // step 1 attends every prompt position
         if (st != ASRKF_OK) return st;
         ctx->lists_ready = true;
     }
+    if (ctx->spill && ctx->xfer_recorded)    // this layer's restored rows are in place
+        HIP_OK(ctx, hipStreamWaitEvent(s, ctx->ev_in[layer], 0));
 
     const size_t inst0 = (size_t)layer * c.batch;
     AttnArgs a{};
-    const size_t pool_off = inst0 * ctx->cap * ctx->row_bytes;
+    const size_t pool_off = inst0 * ctx->pool_rows * ctx->row_bytes;
     a.kpool = (const char*)ctx->kpool + pool_off;
     a.vpool = (const char*)ctx->vpool + pool_off;
     a.kpool_w = (char*)ctx->kpool + pool_off;
@@ -370,6 +557,9 @@ asrkf_status asrkf_decode_step(asrkf_ctx* ctx, int32_t layer, const void* q, con
     a.knew = k_new;
     a.vnew = v_new;
     a.list = ctx->list + inst0 * ctx->cap;
+    a.list_row = ctx->spill ? ctx->list_row + inst0 * ctx->cap : a.list;
+    a.pool_rows = ctx->pool_rows;
+    a.spill = ctx->spill ? 1 : 0;
     a.n_active = ctx->n_active + inst0;
     a.plen = ctx->plen;
     a.unfreeze = ctx->unfreeze + inst0 * ctx->cap;
@@ -426,6 +616,8 @@ asrkf_status asrkf_restore(asrkf_ctx* ctx, const float* logits, asrkf_recover mo
         return fail(ASRKF_ESTATE, "restore before decode_step of every layer (next layer %d of %d)",
                     ctx->next_layer, c.n_layers);
     if ((int)mode < ASRKF_AUTO || (int)mode > ASRKF_NONE) return fail(ASRKF_EINVAL, "unknown recovery mode");
+    st = check_overflow(ctx, false);
+    if (st != ASRKF_OK) return st;
     hipStream_t s = static_cast<hipStream_t>(stream);
     int forced;
     if (logits) {
@@ -487,9 +679,11 @@ asrkf_status asrkf_stats(asrkf_ctx* ctx, asrkf_stats_t* out) {
     if (st != ASRKF_OK) return st;
     st = collect_timing(ctx);
     if (st != ASRKF_OK) return st;
+    st = check_overflow(ctx, true);
+    if (st != ASRKF_OK) return st;
     const asrkf_config& c = ctx->cfg;
     const size_t inst = (size_t)c.n_layers * c.batch;
-    unsigned long long cnt[8];
+    unsigned long long cnt[kCounters];
     std::vector<int32_t> na(inst);
     HIP_OK(ctx, hipMemcpy(cnt, ctx->counters, sizeof cnt, hipMemcpyDeviceToHost));
     HIP_OK(ctx, hipMemcpy(na.data(), ctx->n_active, inst * 4, hipMemcpyDeviceToHost));
@@ -510,6 +704,9 @@ asrkf_status asrkf_stats(asrkf_ctx* ctx, asrkf_stats_t* out) {
     out->attn_launches = ctx->attn_launches;
     out->attn_kernel_ms = ctx->attn_ms_done;
     out->compression = total > 0 ? 1.0 - (double)active / (double)total : 0.0;
+    out->rows_to_host = (int64_t)cnt[8];
+    out->rows_from_host = (int64_t)cnt[9];
+    out->rows_released = (int64_t)cnt[10];
     return ASRKF_OK;
 }
 
@@ -525,7 +722,7 @@ asrkf_status asrkf_stats_reset(asrkf_ctx* ctx) {
     std::vector<int32_t> na(inst);
     HIP_OK(ctx, hipMemcpy(na.data(), ctx->n_active, inst * 4, hipMemcpyDeviceToHost));
     // keep the lists of the coming step counted, drop everything before it
-    unsigned long long cnt[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+    unsigned long long cnt[kCounters] = {};
     if (ctx->lists_ready)
         for (size_t i = 0; i < inst; ++i) cnt[0] += (unsigned long long)na[i];
     HIP_OK(ctx, hipMemcpy(ctx->counters, cnt, sizeof cnt, hipMemcpyHostToDevice));
@@ -552,6 +749,8 @@ asrkf_status asrkf_get_state(asrkf_ctx* ctx, int32_t layer, int32_t seq, int32_t
         return fail(ASRKF_EINVAL, "layer or sequence out of range");
     st = sync_ctx(ctx);
     if (st != ASRKF_OK) return st;
+    st = check_overflow(ctx, true);
+    if (st != ASRKF_OK) return st;
     const int n = ctx->plen_host[seq] + ctx->t;
     const size_t off = ((size_t)layer * c.batch + seq) * ctx->cap;
     std::vector<int32_t> U(n > 0 ? n : 1);
@@ -575,6 +774,32 @@ asrkf_status asrkf_get_state(asrkf_ctx* ctx, int32_t layer, int32_t seq, int32_t
         }
         if (n_active) *n_active = na;
     }
+    return ASRKF_OK;
+}
+
+asrkf_status asrkf_get_residency(asrkf_ctx* ctx, int32_t layer, int32_t seq, int32_t* n_positions,
+                                 int32_t* device_row, uint8_t* on_host) {
+    asrkf_status st = check_ctx(ctx);
+    if (st != ASRKF_OK) return st;
+    const asrkf_config& c = ctx->cfg;
+    if (layer < 0 || layer >= c.n_layers || seq < 0 || seq >= c.batch)
+        return fail(ASRKF_EINVAL, "layer or sequence out of range");
+    st = sync_ctx(ctx);
+    if (st != ASRKF_OK) return st;
+    st = check_overflow(ctx, true);
+    if (st != ASRKF_OK) return st;
+    const int n = ctx->plen_host[seq] + ctx->t;
+    if (n_positions) *n_positions = n;
+    if (n <= 0) return ASRKF_OK;
+    const size_t off = ((size_t)layer * c.batch + seq) * ctx->cap;
+    if (!ctx->spill || !ctx->lists_ready) {
+        // resident mode, or before the first step: every position in its own row
+        if (device_row) for (int p = 0; p < n; ++p) device_row[p] = p;
+        if (on_host) memset(on_host, 0, (size_t)n);
+        return ASRKF_OK;
+    }
+    if (device_row) HIP_OK(ctx, hipMemcpy(device_row, ctx->row_of + off, (size_t)n * 4, hipMemcpyDeviceToHost));
+    if (on_host) HIP_OK(ctx, hipMemcpy(on_host, ctx->on_host + off, (size_t)n, hipMemcpyDeviceToHost));
     return ASRKF_OK;
 }
 

@@ -153,7 +153,8 @@ def run_gpu(w, inp, instances, modes=None, with_logits=True, steps=None, record=
     cfg = A.make_config(w.n_layers, w.batch, w.n_q_heads, w.n_kv_heads, w.head_dim,
                         w.max_ctx, w.window_K, w.tau, w.k_soft, w.vocab,
                         entropy_spike=w.entropy_spike, conf_drop=w.conf_drop,
-                        wr_last_N=w.wr_last_N, dtype=w.dtype)
+                        wr_last_N=w.wr_last_N, dtype=w.dtype, spill_min_D=w.spill_min_D,
+                        device_rows=w.device_rows)
     ctx = A.asrkf_init(cfg)
     res = {key: [] for key in instances}
     seqmon = {b: [] for b in range(w.batch)}
@@ -191,6 +192,8 @@ def run_gpu(w, inp, instances, modes=None, with_logits=True, steps=None, record=
                     st = A.asrkf_get_state(ctx, l, b, w.max_ctx)
                     st["out"] = outs[l][b].cpu().numpy()
                     st["t"] = t
+                    if w.spill_min_D:
+                        st.update(A.asrkf_get_residency(ctx, l, b, w.max_ctx))
                     res[(l, b)].append(st)
                 for b in range(w.batch):
                     seqmon[b].append(A.asrkf_get_seq(ctx, b))
@@ -231,6 +234,34 @@ def compare_instance(gpu_recs, ora_recs, check_out=True):
     return worst
 
 
+def compare_residency(w, gpu_recs, ora_recs):
+    """Spill mode, every step recorded: a position is held only on the host
+    exactly while it is frozen by a freeze of d >= spill_min_D steps (d from
+    its kept count, Eq. 3); resident positions hold distinct device rows; the
+    host store holds every position that was ever released.  Returns the
+    number of (position, step) restores seen."""
+    seen = None
+    restores = 0
+    prev_host_only = None
+    for g, o in zip(gpu_recs, ora_recs):
+        t = o["t"]
+        n = len(o["frozen"])
+        d = np.array([oracle.freeze_duration(int(c), w.k_soft) for c in o["count"]])
+        host_only = o["frozen"] & (d >= w.spill_min_D)
+        row = g["device_row"]
+        np.testing.assert_array_equal(row < 0, host_only, err_msg=f"host-only positions, step {t}")
+        live = row[row >= 0]
+        assert len(np.unique(live)) == len(live), f"device row held twice, step {t}"
+        pool = w.device_rows or (w.max_ctx + 1 + 63) // 64 * 64
+        assert live.size == 0 or (live.min() >= 0 and live.max() < pool), t
+        seen = host_only.copy() if seen is None else np.concatenate([seen, [False] * (n - len(seen))]) | host_only
+        np.testing.assert_array_equal(g["on_host"], seen, err_msg=f"host store contents, step {t}")
+        if prev_host_only is not None:
+            restores += int(np.count_nonzero(prev_host_only & ~host_only[:len(prev_host_only)]))
+        prev_host_only = host_only
+    return restores
+
+
 def run_gpu_device(w, instances, record_steps, seqs_for_entropy=None):
     """Run a large workload exactly as the bench does (device-generated inputs,
     the library's own launch configuration).  Returns per instance the attention
@@ -244,7 +275,8 @@ def run_gpu_device(w, instances, record_steps, seqs_for_entropy=None):
     tdt = torch.bfloat16 if w.dtype == "bf16" else torch.float32
     cfg = A.make_config(L, B, Hq, Hkv, D, w.max_ctx, w.window_K, w.tau, w.k_soft, w.vocab,
                         entropy_spike=w.entropy_spike, conf_drop=w.conf_drop,
-                        wr_last_N=w.wr_last_N, dtype=w.dtype)
+                        wr_last_N=w.wr_last_N, dtype=w.dtype, spill_min_D=w.spill_min_D,
+                        device_rows=w.device_rows)
     ctx = A.asrkf_init(cfg)
     outs = {key: [] for key in instances}
     states = {key: {} for key in instances}
