@@ -221,6 +221,18 @@ def ragged(**kw):
     return Workload(**args)
 
 
+def recovery_stress(**kw):
+    """Recovery stress at the LLaMA-3-8B shape: batch 1, context 131072, spill
+    mode (a token frozen for >= 2 steps leaves the device), entropy trigger at
+    10 nats.  The caller sets ``steps`` and the planted flat-logit step."""
+    args = dict(name="llama3-8b-recovery-ctx131k", seed=SEED + 4, n_layers=1, batch=1,
+                n_q_heads=32, n_kv_heads=8, head_dim=128, dtype="bf16", prefill=[131072],
+                steps=2016, window_K=128, tau=0.5, k_soft=2.0, vocab=128256, logit_sigma=3.0,
+                recipe="hh", f_hh=0.35, entropy_spike=10.0, spill_min_D=2)
+    args.update(kw)
+    return Workload(**args)
+
+
 # --------------------------------------------------------------------------
 # Tensors
 # --------------------------------------------------------------------------
@@ -333,3 +345,53 @@ def hh_relevance_bounds(w):
     beta_min = float(HH_BETA_LO) * (1.0 - 2.0 ** -8)
     s_min_hot = (a_lo - e_axis) * beta_min - off
     return s_max_cold, s_min_hot
+
+
+# --------------------------------------------------------------------------
+# Planted key (recovery stress)
+# --------------------------------------------------------------------------
+
+PLANT_ALPHA = 24.0        # query norm once the queries turn to the planted key
+PLANT_COS = 0.9           # cosine between those queries and the planted key
+
+
+def plant_position(w, layer=0, seq=0, lo=0, hi=65536):
+    """The planted position: the first non-heavy-hitter position at or after a
+    seeded uniform draw in [lo, hi)."""
+    u = float(uniform(draw(subkey(w.seed, KIND_PLANT, layer, seq), U64(0))))
+    p = lo + int(u * (hi - lo))
+    hh = hh_mask(w, layer, seq, p, min(w.prefill[seq], p + 4096))
+    free = np.nonzero(~hh)[0]
+    if len(free) == 0:
+        raise ValueError("no non-heavy-hitter position near the draw")
+    return p + int(free[0])
+
+
+def planted_q_rows(w, k_star, t0, t1, layer=0, seq=0):
+    """Queries of steps t0..t1-1 aimed at the planted key: per head h,
+    alpha * (cos * khat + sqrt(1 - cos^2) * u) with khat the unit key of the
+    head's KV group and u a seeded unit vector orthogonal to khat and to the
+    group's heavy-hitter axis (so heavy-hitter keys do not compete with the
+    planted one).  k_star: [Hkv][D] stored key of the planted position.
+    Returns float32 [t1 - t0][Hq][D] of stored (rounded) values."""
+    Hq, D, G = w.n_q_heads, w.head_dim, w.group
+    kh = np.asarray(k_star, dtype=np.float64)
+    kh = kh / np.linalg.norm(kh, axis=1, keepdims=True)
+    axis, _ = hh_axes(w, layer, seq)
+    key = subkey(w.seed, KIND_PLANT, layer, seq, 1)
+    sine = np.sqrt(1.0 - PLANT_COS ** 2)
+    out = np.empty((t1 - t0, Hq, D), dtype=np.float32)
+    for i, t in enumerate(range(t0, t1)):
+        ctr = U64(t) * U64(Hq * D) + np.arange(Hq * D, dtype=U64)
+        z = gauss(draw(key, ctr)).astype(np.float64).reshape(Hq, D)
+        for h in range(Hq):
+            g = h // G
+            a = np.zeros(D)
+            a[axis[g]] = 1.0
+            e = kh[g]
+            a = a - (a @ e) * e                      # the axis, made orthogonal to khat
+            a /= np.linalg.norm(a)
+            u = z[h] - (z[h] @ e) * e - (z[h] @ a) * a
+            u /= np.linalg.norm(u)
+            out[i, h] = PLANT_ALPHA * (PLANT_COS * e + sine * u)
+    return round_to(out, w.dtype)
