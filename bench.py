@@ -19,7 +19,8 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 PEAK_HBM_GBS = 8000.0
-WORKLOADS = {"32layer": "llama8b_32layer", "1layer": "llama8b_1layer", "ragged": "ragged"}
+WORKLOADS = {"32layer": "llama8b_32layer", "1layer": "llama8b_1layer", "ragged": "ragged",
+             "recovery": "recovery_stress"}
 
 
 def parse():
@@ -115,7 +116,7 @@ def main():
 
     cfg = A.make_config(L, B, Hq, Hkv, D, w.max_ctx, w.window_K, w.tau, w.k_soft, w.vocab,
                         entropy_spike=w.entropy_spike, conf_drop=w.conf_drop,
-                        wr_last_N=w.wr_last_N, dtype=w.dtype)
+                        wr_last_N=w.wr_last_N, dtype=w.dtype, spill_min_D=w.spill_min_D)
     ctx = A.asrkf_init(cfg)
     dg = DeviceGen(w)
     # prompt KV, one (layer, seq) at a time through a staging buffer
@@ -190,7 +191,7 @@ def main():
         "config": {"workload": w.name, "layers": L, "batch": B, "context": w.prefill[0]
                    if len(set(w.prefill)) == 1 else "ragged", "q_heads": Hq, "kv_heads": Hkv,
                    "head_dim": D, "window_K": w.window_K, "tau": w.tau, "k": w.k_soft,
-                   "vocab": w.vocab, "mode": "resident"},
+                   "vocab": w.vocab, "mode": "spill" if w.spill_min_D else "resident"},
         "decode_steps_per_s": K / elapsed,
         "hbm_fraction_step": algo_bytes / elapsed / 1e9 / PEAK_HBM_GBS,
         "attended_fraction": attended / max(1, sum(p + t for p in w.prefill
@@ -206,6 +207,12 @@ def main():
                      "algorithmic_bytes_per_launch": bytes_per_token * attended
                      / max(1, st["attn_launches"])},
     }
+    if w.spill_min_D:
+        row = bytes_per_token // 2                      # one K or V row
+        line["spill"] = {"spill_min_D": w.spill_min_D, "rows_to_host": st["rows_to_host"],
+                         "rows_from_host": st["rows_from_host"],
+                         "h2d_GBps": 2 * row * st["rows_from_host"] / elapsed / 1e9,
+                         "d2h_GBps": 2 * row * st["rows_to_host"] / elapsed / 1e9}
     if args.cpu_seconds > 0:
         line["cpu_baseline"] = cpu_baseline(w, args.cpu_seconds)
     print(json.dumps(line), flush=True)
