@@ -30,6 +30,12 @@ design notes with the evidence for it):
 * the detection count c_j is cumulative (history window W unbounded) and kept
   across restores;
 * entropy is Shannon entropy in nats of softmax(logits), 0 ln 0 = 0;
+* optional readings, each selected explicitly: a finite history window W
+  for c_j (detections in the last W steps, Eq. 3's text); relevance by
+  attention weight (mean over heads of the softmax weights) instead of Eq. 2's
+  |q . k|; token-global scope (one token state per sequence shared by all
+  layers, relevance averaged over layers) instead of per-(layer, sequence)
+  states;
 * recovery (parity unpinned: the paper proposes but never evaluates it):
   a step whose entropy exceeds theta_H (or whose top probability falls below
   theta_p when theta_p > 0) raises the sequence's escalation count by one, a
@@ -105,11 +111,29 @@ def relevance(q, K):
     return s / Hq
 
 
-def attend_rows(q, Kh, Vh):
-    """Eq. 1 and Eq. 2 together over rows given per KV head: Kh[g], Vh[g] are
-    [n][D] arrays of the same n tokens.  The G query heads of a KV head are
-    taken together as one matrix product, so each KV head's rows are read once;
-    the results equal attention() and relevance() up to summation order."""
+def relevance_softmax(q, K):
+    """Relevance by attention weight: s_j = (1/H) sum_h softmax_j(q_h . K_j^(h) / sqrt(d))
+    over the rows of K, H = Hq.  A reading of Eq. 2 under which a token's score
+    is the share of attention it receives, averaged over the heads."""
+    q = np.asarray(q, dtype=np.float64)
+    Hq, D = q.shape
+    group = Hq // K.shape[1]
+    s = np.zeros(K.shape[0])
+    for g in range(K.shape[1]):
+        Kg = np.ascontiguousarray(K[:, g, :], dtype=np.float64)
+        for h in range(g * group, (g + 1) * group):
+            logits = Kg @ q[h] / np.sqrt(D)
+            w = np.exp(logits - logits.max())
+            s += w / w.sum()
+    return s / Hq
+
+
+def attend_rows(q, Kh, Vh, relevance_kind="abs"):
+    """Eq. 1 and the relevance together over rows given per KV head: Kh[g],
+    Vh[g] are [n][D] arrays of the same n tokens.  The G query heads of a KV
+    head are taken together as one matrix product, so each KV head's rows are
+    read once; the results equal attention() and relevance() (or
+    relevance_softmax()) up to summation order."""
     q = np.asarray(q, dtype=np.float64)
     Hq, D = q.shape
     group = Hq // len(Kh)
@@ -120,11 +144,12 @@ def attend_rows(q, Kh, Vh):
         Vg = np.asarray(Vh[g], dtype=np.float64)
         heads = slice(g * group, (g + 1) * group)
         X = Kg @ q[heads].T                        # [n][G]: q_h . k_j
-        for i in range(group):
-            s += np.abs(X[:, i])
         logits = X / np.sqrt(D)
         W = np.exp(logits - logits.max(axis=0))
-        out[heads] = (W / W.sum(axis=0)).T @ Vg
+        W /= W.sum(axis=0)
+        for i in range(group):
+            s += np.abs(X[:, i]) if relevance_kind == "abs" else W[:, i]
+        out[heads] = W.T @ Vg
     return out, s / Hq
 
 
@@ -158,35 +183,31 @@ class StepRecord:
     __slots__ = ("out", "active", "scores")
 
     def __init__(self, out, active, scores):
-        self.out = out          # [Hq][D] attention output of this step
+        self.out = out          # [Hq][D] attention output of this step ([L][Hq][D] token-global)
         self.active = active    # positions attended this step, ascending
         self.scores = scores    # relevance of each attended position
 
 
-class Instance:
-    """Token states of one (layer, sequence): active cache A, frozen storage F,
-    per-token detection count c_j and freeze timer d_j (Algorithm 1 REQUIRE).
-    The cached pairs are kept KV-head major, [Hkv][position][D], in float64."""
+class TokenStates:
+    """Per-token detection count c_j, freeze timer d_j and membership of the
+    frozen storage F (Algorithm 1 REQUIRE), with the freeze loop, the timer
+    loop and the restores of the recovery ladder.
 
-    def __init__(self, K_prompt, V_prompt, window_K, tau, k_soft, capacity=None):
-        K_prompt = np.asarray(K_prompt)
-        V_prompt = np.asarray(V_prompt)
-        P, Hkv, D = K_prompt.shape
-        cap = capacity if capacity is not None else P + 4096
-        # cached pairs, KV-head major: [Hkv][position][D]
-        self.K = np.zeros((Hkv, cap, D))
-        self.V = np.zeros((Hkv, cap, D))
-        self._rows_k = np.empty((Hkv, cap, D))     # the attended rows of one step
-        self._rows_v = np.empty((Hkv, cap, D))
-        self.K[:, :P] = K_prompt.transpose(1, 0, 2)
-        self.V[:, :P] = V_prompt.transpose(1, 0, 2)
-        self.n = P
+    history_W = 0 counts every detection (c_j cumulative); history_W = W > 0
+    counts the detections of the last W steps only (Eq. 3's history window):
+    at a detection in step t, c_j = number of detections in steps t-W+1 .. t."""
+
+    def __init__(self, cap, window_K, tau, k_soft, history_W=0):
+        self.n = 0
+        self.t = 0                                      # current step
         self.window_K = int(window_K)
         self.tau = float(tau)
         self.k_soft = float(k_soft)
+        self.history_W = int(history_W)
         self.count = np.zeros(cap, dtype=np.int64)      # c_j
         self.timer = np.zeros(cap, dtype=np.int64)      # d_j
         self.frozen = np.zeros(cap, dtype=bool)         # membership of F
+        self.detections = [[] for _ in range(cap)] if self.history_W else None
         self._durations = duration_table(64, k_soft)
 
     def _duration(self, c):
@@ -194,43 +215,35 @@ class Instance:
             self._durations = duration_table(2 * len(self._durations), self.k_soft)
         return self._durations[c]
 
+    def _new_position(self, j):
+        self.count[j] = 0
+        self.timer[j] = 0
+        self.frozen[j] = False
+
     def active_positions(self):
         return np.nonzero(~self.frozen[: self.n])[0]
-
-    def step(self, q, k_new, v_new):
-        """One generation step for this layer (Algorithm 1, freeze and timer loops)."""
-        # the new token's KV joins the active cache
-        j_new = self.n
-        self.K[:, j_new] = k_new
-        self.V[:, j_new] = v_new
-        self.count[j_new] = 0
-        self.timer[j_new] = 0
-        self.frozen[j_new] = False
-        self.n += 1
-
-        # Attn(Q_i, A) and relevance s_j for j in A
-        A = self.active_positions()
-        n = len(A)
-        for g in range(self.K.shape[0]):
-            np.take(self.K[g], A, axis=0, out=self._rows_k[g, :n], mode="clip")
-            np.take(self.V[g], A, axis=0, out=self._rows_v[g, :n], mode="clip")
-        out, s = attend_rows(q, self._rows_k[:, :n], self._rows_v[:, :n])
-        self.freeze_loop(A, s)
-        self.timer_loop()
-        return StepRecord(out, A, s)
 
     def outside_window(self, j):
         """True when position j is not among the K most recent positions
         (the window includes the token appended this step)."""
         return j < self.n - self.window_K
 
+    def detect(self, j):
+        """Record a low-relevance detection of j at the current step; returns c_j."""
+        if not self.history_W:
+            self.count[j] += 1
+        else:
+            hist = self.detections[j]
+            hist.append(self.t)
+            self.count[j] = sum(1 for s in hist if s > self.t - self.history_W)
+        return self.count[j]
+
     def freeze_loop(self, A, s):
         """For j outside the sliding window with s_j < tau: c_j += 1,
         d_j = floor(sqrt(c_j)/k), and if d_j > 0 move j from A to F."""
         for j, sj in zip(A, s):
             if self.outside_window(j) and sj < self.tau:
-                self.count[j] += 1
-                self.timer[j] = self._duration(self.count[j])
+                self.timer[j] = self._duration(self.detect(j))
                 if self.timer[j] > 0:
                     self.frozen[j] = True
 
@@ -260,6 +273,97 @@ class Instance:
         """(timers, counts, frozen mask) over the n current positions."""
         n = self.n
         return self.timer[:n].copy(), self.count[:n].copy(), self.frozen[:n].copy()
+
+
+class LayerCache:
+    """The cached pairs (K_j, V_j) of one layer of one sequence, KV-head major
+    [Hkv][position][D] in float64, and Eq. 1 / the relevance over a subset."""
+
+    def __init__(self, K_prompt, V_prompt, cap, relevance_kind="abs"):
+        K_prompt = np.asarray(K_prompt)
+        V_prompt = np.asarray(V_prompt)
+        P, Hkv, D = K_prompt.shape
+        self.K = np.zeros((Hkv, cap, D))
+        self.V = np.zeros((Hkv, cap, D))
+        self._rows_k = np.empty((Hkv, cap, D))     # the attended rows of one step
+        self._rows_v = np.empty((Hkv, cap, D))
+        self.K[:, :P] = K_prompt.transpose(1, 0, 2)
+        self.V[:, :P] = V_prompt.transpose(1, 0, 2)
+        self.relevance_kind = relevance_kind
+
+    def put(self, j, k_new, v_new):
+        self.K[:, j] = k_new
+        self.V[:, j] = v_new
+
+    def attend(self, q, A):
+        """Attn(q, A) and the relevance of every j in A."""
+        n = len(A)
+        for g in range(self.K.shape[0]):
+            np.take(self.K[g], A, axis=0, out=self._rows_k[g, :n], mode="clip")
+            np.take(self.V[g], A, axis=0, out=self._rows_v[g, :n], mode="clip")
+        return attend_rows(q, self._rows_k[:, :n], self._rows_v[:, :n], self.relevance_kind)
+
+
+class Instance(TokenStates):
+    """Token states of one (layer, sequence): active cache A, frozen storage F,
+    per-token detection count c_j and freeze timer d_j (Algorithm 1 REQUIRE).
+    relevance_kind "abs" is Eq. 2; "softmax" scores by attention weights."""
+
+    def __init__(self, K_prompt, V_prompt, window_K, tau, k_soft, capacity=None,
+                 history_W=0, relevance_kind="abs"):
+        P = len(K_prompt)
+        cap = capacity if capacity is not None else P + 4096
+        super().__init__(cap, window_K, tau, k_soft, history_W)
+        self.cache = LayerCache(K_prompt, V_prompt, cap, relevance_kind)
+        self.K, self.V = self.cache.K, self.cache.V
+        self.n = P
+
+    def step(self, q, k_new, v_new):
+        """One generation step for this layer (Algorithm 1, freeze and timer loops)."""
+        self.t += 1
+        j_new = self.n
+        self.cache.put(j_new, k_new, v_new)
+        self._new_position(j_new)
+        self.n += 1
+        A = self.active_positions()
+        out, s = self.cache.attend(q, A)
+        self.freeze_loop(A, s)
+        self.timer_loop()
+        return StepRecord(out, A, s)
+
+
+class GlobalInstance(TokenStates):
+    """Token-global scope: one set of token states per sequence, shared by
+    all layers (a token's KV pair leaves every layer at once, Sec. 3.2).  The
+    relevance of a token is the mean of its per-layer relevance (each a mean
+    over that layer's heads), i.e. the mean over layers x heads."""
+
+    def __init__(self, K_prompts, V_prompts, window_K, tau, k_soft, capacity=None,
+                 history_W=0, relevance_kind="abs"):
+        P = len(K_prompts[0])
+        cap = capacity if capacity is not None else P + 4096
+        super().__init__(cap, window_K, tau, k_soft, history_W)
+        self.caches = [LayerCache(K, V, cap, relevance_kind) for K, V in zip(K_prompts, V_prompts)]
+        self.n = P
+
+    def step(self, qs, k_news, v_news):
+        """One generation step of every layer: qs, k_news, v_news indexed by layer."""
+        self.t += 1
+        j_new = self.n
+        for cache, k, v in zip(self.caches, k_news, v_news):
+            cache.put(j_new, k, v)
+        self._new_position(j_new)
+        self.n += 1
+        A = self.active_positions()
+        outs, s = [], np.zeros(len(A))
+        for cache, q in zip(self.caches, qs):
+            o, sl = cache.attend(q, A)
+            outs.append(o)
+            s += sl
+        s /= len(self.caches)
+        self.freeze_loop(A, s)
+        self.timer_loop()
+        return StepRecord(np.stack(outs), A, s)
 
 
 # ---------------------------------------------------------------------------

@@ -202,6 +202,7 @@ def test_recovery_stress_ctx131k():
     n = P + t_s - 1
     inst = oracle.Instance(K[:n], V[:n], Kw, w.tau, w.k_soft, capacity=P + S + 1)
     inst.count[:n], inst.frozen[:n], inst.timer[:n] = cnt, fz, tm
+    inst.t = t_s - 1
     for t in range(t_s, S + 1):
         rec = inst.step(q_of(t), K[P + t - 1], V[P + t - 1])
         if levels[t - 1]:
