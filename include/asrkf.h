@@ -58,6 +58,12 @@ typedef enum {
     ASRKF_NONE = 4    /* no recovery; entropy is still computed when logits are given */
 } asrkf_recover;
 
+/* Relevance score used by the freeze loop. */
+typedef enum { ASRKF_REL_ABS = 0, ASRKF_REL_SOFTMAX = 1 } asrkf_relevance;
+
+/* Scope of the token states. */
+typedef enum { ASRKF_SCOPE_LAYER = 0, ASRKF_SCOPE_TOKEN = 1 } asrkf_scope;
+
 typedef struct {
     int32_t n_layers;        /* >= 1 */
     int32_t batch;           /* sequences, 1 .. 1024 */
@@ -86,6 +92,16 @@ typedef struct {
                                 sequence that needs more rows than this voids the results
                                 and the next call returns ECAPACITY.  Must be 0 in
                                 resident mode. */
+    int32_t history_W;       /* window of the detection count c_j (Eq. 3's history window W):
+                                0 counts every detection; 1 .. 64 counts the detections of
+                                the last history_W steps */
+    int32_t relevance;       /* ASRKF_REL_ABS: Eq. 2, s_j = (1/H) sum_h |q_h . k_j|;
+                                ASRKF_REL_SOFTMAX: s_j = (1/H) sum_h softmax weight of j
+                                under head h (the share of attention j receives) */
+    int32_t scope;           /* ASRKF_SCOPE_LAYER: token states per (layer, sequence);
+                                ASRKF_SCOPE_TOKEN: one token state per sequence shared by
+                                every layer (a frozen token leaves all layers), scored by
+                                the mean of its per-layer relevance.  Not with spill mode. */
 } asrkf_config;
 
 typedef struct {
@@ -160,7 +176,8 @@ asrkf_status asrkf_stats_reset(asrkf_ctx* ctx);
 asrkf_status asrkf_set_timing(asrkf_ctx* ctx, int32_t enable);
 
 /* Token states of one (layer, sequence) after the last completed step t
- * (test export).  All outputs are host buffers of at least max_ctx entries
+ * (test export; with ASRKF_SCOPE_TOKEN every layer shows the sequence's one
+ * state).  All outputs are host buffers of at least max_ctx entries
  * (any may be NULL):
  *   n_positions:   receives n_t
  *   unfreeze_step: [n_t] step at which a frozen token attends again

@@ -16,6 +16,8 @@ LIB_PATH = os.path.join(HERE, "libasrkf.so")
 OK, EINVAL, ENOMEM, EHIP, ESTATE, ECAPACITY = 0, -1, -2, -3, -4, -5
 BF16, F32 = 0, 1
 AUTO, SR, WR, FR, NONE = 0, 1, 2, 3, 4
+REL_ABS, REL_SOFTMAX = 0, 1
+SCOPE_LAYER, SCOPE_TOKEN = 0, 1
 _STATUS = {EINVAL: "EINVAL", ENOMEM: "ENOMEM", EHIP: "EHIP", ESTATE: "ESTATE",
            ECAPACITY: "ECAPACITY"}
 
@@ -29,7 +31,8 @@ class asrkf_config(ctypes.Structure):
         ("vocab", ctypes.c_int32), ("entropy_spike", ctypes.c_float),
         ("conf_drop", ctypes.c_float), ("wr_last_N", ctypes.c_int32),
         ("dtype", ctypes.c_int32), ("spill_min_D", ctypes.c_int32),
-        ("device_rows", ctypes.c_int32),
+        ("device_rows", ctypes.c_int32), ("history_W", ctypes.c_int32),
+        ("relevance", ctypes.c_int32), ("scope", ctypes.c_int32),
     ]
 
 
@@ -118,10 +121,13 @@ def _stream(s):
 
 def make_config(n_layers, batch, n_q_heads, n_kv_heads, head_dim, max_ctx, window_K, tau,
                 k_soft, vocab, entropy_spike=math.inf, conf_drop=0.0, wr_last_N=0,
-                dtype="bf16", spill_min_D=0, device_rows=0):
+                dtype="bf16", spill_min_D=0, device_rows=0, history_W=0, relevance="abs",
+                scope="layer"):
     return asrkf_config(n_layers, batch, n_q_heads, n_kv_heads, head_dim, max_ctx, window_K,
                         tau, k_soft, vocab, entropy_spike, conf_drop, wr_last_N,
-                        BF16 if dtype == "bf16" else F32, spill_min_D, device_rows)
+                        BF16 if dtype == "bf16" else F32, spill_min_D, device_rows, history_W,
+                        REL_SOFTMAX if relevance == "softmax" else REL_ABS,
+                        SCOPE_TOKEN if scope == "token" else SCOPE_LAYER)
 
 
 def asrkf_init(cfg):

@@ -7,7 +7,7 @@ import tempfile
 HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libasrkf.so")
-SOURCES = ["attention.hip", "compact.hip", "entropy.hip", "xfer.hip", "runtime.hip"]
+SOURCES = ["attention.hip", "relevance.hip", "compact.hip", "entropy.hip", "xfer.hip", "runtime.hip"]
 ARCH = "gfx950"
 # no packed fp32 instructions anywhere in the device code
 DEVICE_FLAGS = ["-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"]

@@ -246,6 +246,8 @@ attention_kernel(AttnArgs a) {
         const int32_t* list_b = a.list + seq_row;
         const int32_t* lrow_b = a.list_row + seq_row;
         const bool spill = a.spill != 0;
+        const bool rel_abs = a.rel_mode == 0;
+        const bool scope_token = a.scope_token != 0;
 
         uint4 qr[G][NC];
         {
@@ -331,17 +333,26 @@ attention_kernel(AttnArgs a) {
 #pragma unroll
                     for (int h = 0; h < G; ++h) xs[u][h] += dpp_mov<0x141>(xs[u][h]);  // row_half_mirror
 
-                // relevance: sum over the slot's heads, then over the token's KV-head slots
+                // relevance (Eq. 2): sum over the slot's heads, then over the token's KV-head slots
+                if (rel_abs) {
 #pragma unroll
-                for (int u = 0; u < kUnroll; ++u) {
-                    float rel = 0.f;
+                    for (int u = 0; u < kUnroll; ++u) {
+                        float rel = 0.f;
 #pragma unroll
-                    for (int h = 0; h < G; ++h) rel += fabsf(xs[u][h]);
-                    if constexpr (HKV >= 2) rel += lane_xor<8>(rel);
-                    if constexpr (HKV >= 4) rel += lane_xor<16>(rel);
-                    if constexpr (HKV >= 8) rel += lane_xor<32>(rel);
-                    if (valid[u] && g == 0 && r == 0 && pos[u] < wedge && rel < a.tau_H)
-                        flag_lds[tb + u * TPI + tk] = 1;
+                        for (int h = 0; h < G; ++h) rel += fabsf(xs[u][h]);
+                        if constexpr (HKV >= 2) rel += lane_xor<8>(rel);
+                        if constexpr (HKV >= 4) rel += lane_xor<16>(rel);
+                        if constexpr (HKV >= 8) rel += lane_xor<32>(rel);
+                        if (valid[u] && g == 0 && r == 0) {
+                            if (scope_token) {
+                                // summed over layers here, the freeze loop runs at the step's end
+                                float* ra = a.rel_acc + seq_row + pos[u];
+                                *ra = a.first_layer ? rel : *ra + rel;
+                            } else if (pos[u] < wedge && rel < a.tau_H) {
+                                flag_lds[tb + u * TPI + tk] = 1;
+                            }
+                        }
+                    }
                 }
 
                 float y[kUnroll][G];
@@ -349,6 +360,17 @@ attention_kernel(AttnArgs a) {
                 for (int u = 0; u < kUnroll; ++u)
 #pragma unroll
                     for (int h = 0; h < G; ++h) y[u][h] = valid[u] ? xs[u][h] * a.scale_log2 : -INFINITY;
+                if (!rel_abs) {
+                    // relevance by attention weight needs the sequence's normaliser: keep the logits
+#pragma unroll
+                    for (int u = 0; u < kUnroll; ++u) {
+                        if (valid[u] && r == 0) {
+                            float* xl = a.xlog + (seq_row + c0 + tb + u * TPI + tk) * a.Hq + g * G;
+#pragma unroll
+                            for (int h = 0; h < G; ++h) xl[h] = y[u][h];
+                        }
+                    }
+                }
 #pragma unroll
                 for (int h = 0; h < G; ++h) {
                     float mt = st.m[h];
@@ -378,8 +400,7 @@ attention_kernel(AttnArgs a) {
             for (int i = threadIdx.x; i < len; i += blockDim.x) {
                 if (!flag_lds[i]) continue;
                 const size_t o = seq_row + pos_lds[i];
-                const int c = a.count[o] + 1;
-                a.count[o] = c;
+                const int c = detect(a.count, a.hmask, a.hlast, o, a.t, a.history_W);
                 const int d = c < kDurCache ? dur_lds[c] : a.dur[min(c, a.dur_len - 1)];
                 if (d >= 1) a.unfreeze[o] = a.t + d;
             }
@@ -531,6 +552,10 @@ finish_kernel(FinishArgs a, int D) {
             lt += redl[k * kFinishDims + threadIdx.x];
         }
         a.out[(size_t)bh * D + d] = o / lt;
+        if (a.norm && threadIdx.x == 0 && blockIdx.x % per_head == 0) {
+            a.norm[(size_t)bh * 2] = M;
+            a.norm[(size_t)bh * 2 + 1] = lt;
+        }
     }
 }
 

@@ -1,7 +1,10 @@
 // End-of-step rebuild of every active cache, with staged recovery fused in.
 //
-// One workgroup per (layer, sequence).  It streams the unfreeze steps U_p of
-// the n_t positions and:
+// One workgroup per (layer, sequence), or per sequence when the token states
+// are shared by all layers.  It streams the unfreeze steps U_p of the n_t
+// positions and:
+//   0. token scope only: runs the step's freeze loop (Algorithm 1) on the
+//      relevance summed over all layers, since no single layer can;
 //   1. applies the recovery level chosen for the sequence (Sec. 3.6):
 //        SR: remaining timer U_p - (t+1) > 1     ->  U_p = t+1
 //        WR: p >= n_t - N and U_p > t+1          ->  U_p = t+1
@@ -116,8 +119,9 @@ compact_kernel(CompactArgs a) {
     const int b = inst % a.B;
     const int n = a.plen[b] + a.t;            // positions after step t
     const Ladder r = make_ladder(a, b, n);
-    int32_t* U = a.unfreeze + (size_t)inst * a.cap;
-    int32_t* list = a.list + (size_t)inst * a.cap;
+    const size_t base = (size_t)inst * a.cap;
+    int32_t* U = a.unfreeze + base;
+    int32_t* list = a.list + base;
     const int tid = threadIdx.x;
     int listed = 0;
 
@@ -127,6 +131,22 @@ compact_kernel(CompactArgs a) {
         load4(U, p, n, u, 0);
         bool flag[4];
         bool dirty = false;
+        if (a.scope_token) {
+            // token scope: Algorithm 1's freeze loop for the whole sequence, on the
+            // relevance summed over every layer's heads (state before this step: U <= t attended)
+#pragma unroll
+            for (int k = 0; k < 4; ++k) {
+                const int q = p + k;
+                if (q < n && u[k] <= a.t && q < n - a.window_K && a.rel_acc[base + q] < a.tau_LH) {
+                    const int c = detect(a.count, a.hmask, a.hlast, base + q, a.t, a.history_W);
+                    const int d = a.dur[min(c, a.dur_len - 1)];
+                    if (d >= 1) {
+                        u[k] = a.t + d;
+                        dirty = true;
+                    }
+                }
+            }
+        }
 #pragma unroll
         for (int k = 0; k < 4; ++k) {
             bool hit;

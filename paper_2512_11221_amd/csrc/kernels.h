@@ -14,6 +14,27 @@ namespace asrkf {
 // its range touches, at slot (workgroup + sequence).
 constexpr int kMaxBatch = 1024;
 
+// A low-relevance detection of the token at state index o in step t: the new
+// count c_j (Eq. 3).  W = 0 counts every detection; otherwise a bit mask of
+// the detections of the last W steps (bit i = step t - i) gives the count.
+__device__ __forceinline__ int detect(int32_t* count, uint64_t* hmask, int32_t* hlast, size_t o,
+                                      int t, int W) {
+    int c;
+    if (W == 0) {
+        c = count[o] + 1;
+    } else {
+        const int gap = t - hlast[o];
+        uint64_t m = gap >= 64 ? 0ull : (hmask[o] << gap);
+        m |= 1ull;
+        if (W < 64) m &= (1ull << W) - 1ull;
+        hmask[o] = m;
+        hlast[o] = t;
+        c = __popcll(m);
+    }
+    count[o] = c;
+    return c;
+}
+
 struct AttnArgs {
     const void* kpool;        // layer base, [B][pool_rows][Hkv][D]
     const void* vpool;
@@ -42,6 +63,15 @@ struct AttnArgs {
     int32_t dur_len;
     float tau_H;              // tau * Hq: compared against sum_h |q_h . k_j|
     float scale_log2;         // log2(e) / sqrt(D)
+    // relevance reading and state scope
+    int32_t rel_mode;         // 0: Eq. 2 |q.k| scored here; 1: softmax weights (weight_relevance_kernel)
+    int32_t scope_token;      // 1: one token state per sequence; the freeze loop runs at the step's end
+    int32_t first_layer;      // token scope: this launch starts the per-token sums
+    int32_t history_W;        // 0: cumulative detection count; else window in steps
+    uint64_t* hmask;          // state base [B][cap] (history window): detection bits, bit i = step hlast - i
+    int32_t* hlast;           // state base [B][cap]: step of the last detection
+    float* rel_acc;           // token scope, [B][cap]: sum over layers and heads of the relevance
+    float* xlog;              // softmax relevance, [B][cap][Hq]: q.k * log2(e)/sqrt(D) per listed token
 };
 
 // Per layer, after the attention: the split combine of Eq. 1.
@@ -51,7 +81,27 @@ struct FinishArgs {
     const int32_t* slot_first;
     const int32_t* slot_end;
     float* out;               // [B][Hq][D]
+    float* norm;              // softmax relevance: [B][Hq][2] (max, sum) of the sequence (written), or null
     int32_t B, Hq;
+};
+
+// Relevance by attention weight, after the split combine of a layer:
+// s_j = sum_h 2^(y_hj - M_h) / L_h over the heads (compared with tau * Hq),
+// then the freeze loop (layer scope) or the per-token sum (token scope).
+struct RelevanceArgs {
+    const float* xlog;        // [B][cap][Hq]
+    const float* norm;        // [B][Hq][2]
+    const int32_t* list;      // state base [B][cap]
+    const int32_t* n_active;  // state base [B]
+    const int32_t* plen;
+    int32_t* unfreeze;        // state base [B][cap]
+    int32_t* count;
+    uint64_t* hmask;
+    int32_t* hlast;
+    const int32_t* dur;
+    float* rel_acc;           // token scope [B][cap]
+    int32_t B, cap, Hq, t, window_K, dur_len, history_W, scope_token, first_layer;
+    float tau_H;
 };
 
 struct CompactArgs {
@@ -80,6 +130,15 @@ struct CompactArgs {
     int32_t* n_in;            // [L][B]
     int32_t* overflow;        // set to 1 when a sequence needs more device rows than it has
     unsigned long long* xfer; // [0] rows to host, [1] rows from host, [2] device rows released
+    // token scope: the freeze loop of the step runs here, before recovery
+    int32_t scope_token;
+    const float* rel_acc;     // [B][cap] relevance summed over layers and heads
+    float tau_LH;             // tau * n_layers * Hq
+    int32_t* count;           // [B][cap]
+    uint64_t* hmask;
+    int32_t* hlast;
+    const int32_t* dur;
+    int32_t dur_len, history_W, window_K;
 };
 
 // First decode step in spill mode: prompt positions p < P sit in device rows
@@ -131,6 +190,7 @@ hipError_t attention_occupancy(const AttnArgs& a, int dtype_bf16, int head_dim, 
                                int* blocks_per_cu);
 hipError_t launch_finish(const FinishArgs& a, int head_dim, hipStream_t s);
 hipError_t launch_compact(const CompactArgs& a, int n_instances, hipStream_t s);
+hipError_t launch_weight_relevance(const RelevanceArgs& a, hipStream_t s);
 hipError_t launch_spill_init(const SpillInitArgs& a, int n_instances, hipStream_t s);
 hipError_t launch_xfer(const XferArgs& a, int n_instances, hipStream_t s);
 hipError_t launch_entropy(const EntropyArgs& a, hipStream_t s);

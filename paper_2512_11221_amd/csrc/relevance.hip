@@ -1,0 +1,55 @@
+// Relevance by attention weight (the softmax reading of Eq. 2): a token's
+// score is the share of attention it received, averaged over the heads,
+//     s_j = (1/H) sum_h softmax_j(q_h . k_j / sqrt(d)),
+// which needs each head's normaliser over the whole active set.  The
+// attention kernel keeps y_hj = q_h . k_j * log2(e)/sqrt(d) of every listed
+// token, the split combine leaves (M_h, L_h) = (max, sum of 2^(y - M)), and
+// this kernel forms H * s_j = sum_h 2^(y_hj - M_h) / L_h.  It then runs the
+// freeze loop of Algorithm 1 for the layer (layer scope) or adds the score to
+// the token's sum over layers (token scope; the freeze loop runs at the end
+// of the step).  One thread per listed token.
+#include "kernels.h"
+
+namespace asrkf {
+namespace {
+
+constexpr int kThreads = 256;
+constexpr int kMaxHeads = 256;
+
+__global__ void __launch_bounds__(kThreads)
+weight_relevance_kernel(RelevanceArgs a) {
+    __shared__ float M[kMaxHeads], invL[kMaxHeads];
+    const int b = blockIdx.y;
+    for (int h = threadIdx.x; h < a.Hq; h += kThreads) {
+        M[h] = a.norm[((size_t)b * a.Hq + h) * 2];
+        invL[h] = 1.f / a.norm[((size_t)b * a.Hq + h) * 2 + 1];
+    }
+    __syncthreads();
+    const int n = a.n_active[b];
+    const int wedge = a.plen[b] + a.t - a.window_K;     // positions < wedge are outside the window
+    const size_t row = (size_t)b * a.cap;
+    for (int i = blockIdx.x * kThreads + threadIdx.x; i < n; i += gridDim.x * kThreads) {
+        const float* y = a.xlog + (row + i) * a.Hq;
+        float s = 0.f;
+        for (int h = 0; h < a.Hq; ++h) s = fmaf(__builtin_amdgcn_exp2f(y[h] - M[h]), invL[h], s);
+        const int pos = a.list[row + i];
+        const size_t o = row + pos;
+        if (a.scope_token) {
+            a.rel_acc[o] = a.first_layer ? s : a.rel_acc[o] + s;
+        } else if (pos < wedge && s < a.tau_H) {
+            const int c = detect(a.count, a.hmask, a.hlast, o, a.t, a.history_W);
+            const int d = a.dur[min(c, a.dur_len - 1)];
+            if (d >= 1) a.unfreeze[o] = a.t + d;
+        }
+    }
+}
+
+}  // namespace
+
+hipError_t launch_weight_relevance(const RelevanceArgs& a, hipStream_t s) {
+    if (a.Hq > kMaxHeads) return hipErrorInvalidValue;
+    hipLaunchKernelGGL(weight_relevance_kernel, dim3(64, a.B), dim3(kThreads), 0, s, a);
+    return hipGetLastError();
+}
+
+}  // namespace asrkf

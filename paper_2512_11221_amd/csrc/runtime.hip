@@ -105,6 +105,15 @@ struct asrkf_ctx {
     unsigned long long* counters = nullptr;   // [0] listed_total, [1..3] recoveries, [5] rr,
                                               // [8] rows to host, [9] rows from host, [10] released
 
+    // relevance reading and state scope
+    bool token_scope = false;     // one token state per sequence (state_layers = 1)
+    int state_layers = 0;         // layers that own token states: n_layers, or 1
+    uint64_t* hmask = nullptr;    // [state_layers][B][cap] (history window)
+    int32_t* hlast = nullptr;
+    float* rel_acc = nullptr;     // [B][cap] (token scope)
+    float* xlog = nullptr;        // [B][cap][Hq] (relevance by attention weight)
+    float* norm = nullptr;        // [B][Hq][2]
+
     // spill mode
     bool spill = false;
     int pool_rows = 0;            // device rows per (layer, seq)
@@ -185,7 +194,8 @@ void free_all(asrkf_ctx* ctx) {
                     ctx->entropy, ctx->pmax, ctx->part_acc, ctx->part_ml, ctx->slot_info, ctx->ent_partial, ctx->ent_ticket,
                     ctx->counters, ctx->row_of, ctx->on_host, ctx->list_row, ctx->free_rows,
                     ctx->free_top, ctx->out_pos, ctx->out_row, ctx->n_out, ctx->in_pos, ctx->in_row,
-                    ctx->n_in, ctx->overflow};
+                    ctx->n_in, ctx->overflow, ctx->hmask, ctx->hlast, ctx->rel_acc, ctx->xlog,
+                    ctx->norm};
     for (void* p : ptrs) if (p) (void)hipFree(p);
     void* host[] = {ctx->khost, ctx->vhost, ctx->overflow_host};
     for (void* p : host) if (p) (void)hipHostFree(p);
@@ -216,6 +226,13 @@ asrkf_status validate(const asrkf_config* c) {
     if (isnan(c->entropy_spike) || isnan(c->conf_drop)) return fail(ASRKF_EINVAL, "NaN threshold");
     if (c->dtype != ASRKF_BF16 && c->dtype != ASRKF_F32) return fail(ASRKF_EINVAL, "unknown dtype");
     if (c->spill_min_D < 0) return fail(ASRKF_EINVAL, "spill_min_D must be >= 0");
+    if (c->history_W < 0 || c->history_W > 64) return fail(ASRKF_EINVAL, "history_W must be in 0..64");
+    if (c->relevance != ASRKF_REL_ABS && c->relevance != ASRKF_REL_SOFTMAX)
+        return fail(ASRKF_EINVAL, "unknown relevance kind");
+    if (c->scope != ASRKF_SCOPE_LAYER && c->scope != ASRKF_SCOPE_TOKEN)
+        return fail(ASRKF_EINVAL, "unknown state scope");
+    if (c->scope == ASRKF_SCOPE_TOKEN && c->spill_min_D != 0)
+        return fail(ASRKF_EINVAL, "spill mode needs per-layer token states (ASRKF_SCOPE_LAYER)");
     if (c->spill_min_D == 0 && c->device_rows != 0)
         return fail(ASRKF_EINVAL, "device_rows applies to spill mode only (spill_min_D > 0)");
     if (c->device_rows != 0 && (c->device_rows < 2 || c->device_rows > c->max_ctx + 1))
@@ -285,8 +302,12 @@ asrkf_status asrkf_init(const asrkf_config* cfg, asrkf_ctx** out) {
     ctx->spill = c.spill_min_D > 0;
     ctx->pool_rows = ctx->spill && c.device_rows > 0 ? c.device_rows : ctx->cap;
 
-    const size_t inst = (size_t)c.n_layers * c.batch;
+    ctx->token_scope = c.scope == ASRKF_SCOPE_TOKEN;
+    ctx->state_layers = ctx->token_scope ? 1 : c.n_layers;
+    const size_t inst = (size_t)c.n_layers * c.batch;          // (layer, sequence) caches
     const size_t per_pos = inst * ctx->cap;
+    const size_t st_inst = (size_t)ctx->state_layers * c.batch; // token-state instances
+    const size_t st_pos = st_inst * ctx->cap;
 #define ALLOC(field, bytes)                                       \
     do {                                                          \
         st = dev_alloc(ctx, &ctx->field, (bytes));                \
@@ -295,9 +316,18 @@ asrkf_status asrkf_init(const asrkf_config* cfg, asrkf_ctx** out) {
     const size_t pool_bytes = inst * ctx->pool_rows * ctx->row_bytes;
     ALLOC(kpool, pool_bytes);
     ALLOC(vpool, pool_bytes);
-    ALLOC(unfreeze, per_pos * 4);
-    ALLOC(count, per_pos * 4);
-    ALLOC(list, per_pos * 4);
+    ALLOC(unfreeze, st_pos * 4);
+    ALLOC(count, st_pos * 4);
+    ALLOC(list, st_pos * 4);
+    if (c.history_W > 0) {
+        ALLOC(hmask, st_pos * 8);
+        ALLOC(hlast, st_pos * 4);
+    }
+    if (ctx->token_scope) ALLOC(rel_acc, (size_t)c.batch * ctx->cap * 4);
+    if (c.relevance == ASRKF_REL_SOFTMAX) {
+        ALLOC(xlog, (size_t)c.batch * ctx->cap * c.n_q_heads * 4);
+        ALLOC(norm, (size_t)c.batch * c.n_q_heads * 2 * 4);
+    }
     ALLOC(n_active, inst * 4);
     ALLOC(plen, (size_t)c.batch * 4);
     ALLOC(dur, (size_t)ctx->dur_len * 4);
@@ -361,9 +391,11 @@ asrkf_status asrkf_init(const asrkf_config* cfg, asrkf_ctx** out) {
         hipError_t e_ = (expr);                                                 \
         if (e_ != hipSuccess) { st = hip_fail(nullptr, e_, #expr); free_all(ctx); delete ctx; return st; } \
     } while (0)
-    INIT(hipMemset(ctx->unfreeze, 0, per_pos * 4));
-    INIT(hipMemset(ctx->count, 0, per_pos * 4));
-    INIT(hipMemset(ctx->n_active, 0, inst * 4));
+    INIT(hipMemset(ctx->unfreeze, 0, st_pos * 4));
+    INIT(hipMemset(ctx->count, 0, st_pos * 4));
+    INIT(hipMemset(ctx->n_active, 0, st_inst * 4));
+    if (ctx->hmask) INIT(hipMemset(ctx->hmask, 0, st_pos * 8));
+    if (ctx->hlast) INIT(hipMemset(ctx->hlast, 0, st_pos * 4));
     INIT(hipMemset(ctx->plen, 0, (size_t)c.batch * 4));
     INIT(hipMemset(ctx->escalation, 0, (size_t)c.batch * 4));
     INIT(hipMemset(ctx->level, 0, (size_t)c.batch * 4));
@@ -415,7 +447,7 @@ asrkf_status asrkf_prefill(asrkf_ctx* ctx, int32_t layer, int32_t seq, const voi
 namespace {
 
 asrkf_status build_lists(asrkf_ctx* ctx, int forced_level, hipStream_t s) {
-    const int n_inst = ctx->cfg.n_layers * ctx->cfg.batch;
+    const int n_inst = ctx->state_layers * ctx->cfg.batch;
     if (ctx->spill && ctx->t == 0) {
         SpillInitArgs z{};
         z.row_of = ctx->row_of;
@@ -440,6 +472,18 @@ asrkf_status build_lists(asrkf_ctx* ctx, int forced_level, hipStream_t s) {
     a.B = ctx->cfg.batch;
     a.cap = ctx->cap;
     a.wr_last_N = ctx->cfg.wr_last_N;
+    if (ctx->token_scope && ctx->t > 0) {    // the step's freeze loop (not before the first step)
+        a.scope_token = 1;
+        a.rel_acc = ctx->rel_acc;
+        a.tau_LH = ctx->cfg.tau * (float)ctx->cfg.n_layers * (float)ctx->cfg.n_q_heads;
+        a.count = ctx->count;
+        a.hmask = ctx->hmask;
+        a.hlast = ctx->hlast;
+        a.dur = ctx->dur;
+        a.dur_len = ctx->dur_len;
+        a.history_W = ctx->cfg.history_W;
+        a.window_K = ctx->cfg.window_K;
+    }
     if (ctx->spill) {
         a.spill_min_D = ctx->cfg.spill_min_D;
         a.pool_rows = ctx->pool_rows;
@@ -546,7 +590,8 @@ asrkf_status asrkf_decode_step(asrkf_ctx* ctx, int32_t layer, const void* q, con
     if (ctx->spill && ctx->xfer_recorded)    // this layer's restored rows are in place
         HIP_OK(ctx, hipStreamWaitEvent(s, ctx->ev_in[layer], 0));
 
-    const size_t inst0 = (size_t)layer * c.batch;
+    const size_t inst0 = (size_t)layer * c.batch;              // this layer's caches
+    const size_t st0 = ctx->token_scope ? 0 : inst0;           // its token states
     AttnArgs a{};
     const size_t pool_off = inst0 * ctx->pool_rows * ctx->row_bytes;
     a.kpool = (const char*)ctx->kpool + pool_off;
@@ -556,14 +601,22 @@ asrkf_status asrkf_decode_step(asrkf_ctx* ctx, int32_t layer, const void* q, con
     a.q = q;
     a.knew = k_new;
     a.vnew = v_new;
-    a.list = ctx->list + inst0 * ctx->cap;
+    a.list = ctx->list + st0 * ctx->cap;
     a.list_row = ctx->spill ? ctx->list_row + inst0 * ctx->cap : a.list;
     a.pool_rows = ctx->pool_rows;
     a.spill = ctx->spill ? 1 : 0;
-    a.n_active = ctx->n_active + inst0;
+    a.n_active = ctx->n_active + st0;
     a.plen = ctx->plen;
-    a.unfreeze = ctx->unfreeze + inst0 * ctx->cap;
-    a.count = ctx->count + inst0 * ctx->cap;
+    a.unfreeze = ctx->unfreeze + st0 * ctx->cap;
+    a.count = ctx->count + st0 * ctx->cap;
+    a.hmask = ctx->hmask ? ctx->hmask + st0 * ctx->cap : nullptr;
+    a.hlast = ctx->hlast ? ctx->hlast + st0 * ctx->cap : nullptr;
+    a.history_W = c.history_W;
+    a.rel_mode = c.relevance;
+    a.scope_token = ctx->token_scope ? 1 : 0;
+    a.first_layer = layer == 0 ? 1 : 0;
+    a.rel_acc = ctx->rel_acc;
+    a.xlog = ctx->xlog;
     a.dur = ctx->dur;
     a.part_acc = ctx->part_acc;
     a.part_ml = ctx->part_ml;
@@ -599,9 +652,35 @@ asrkf_status asrkf_decode_step(asrkf_ctx* ctx, int32_t layer, const void* q, con
     f.slot_first = a.slot_first;
     f.slot_end = a.slot_end;
     f.out = out;
+    f.norm = ctx->norm;
     f.B = c.batch;
     f.Hq = c.n_q_heads;
     HIP_OK(ctx, launch_finish(f, c.head_dim, s));
+    if (c.relevance == ASRKF_REL_SOFTMAX) {
+        RelevanceArgs r{};
+        r.xlog = ctx->xlog;
+        r.norm = ctx->norm;
+        r.list = a.list;
+        r.n_active = a.n_active;
+        r.plen = ctx->plen;
+        r.unfreeze = a.unfreeze;
+        r.count = a.count;
+        r.hmask = a.hmask;
+        r.hlast = a.hlast;
+        r.dur = ctx->dur;
+        r.rel_acc = ctx->rel_acc;
+        r.B = c.batch;
+        r.cap = ctx->cap;
+        r.Hq = c.n_q_heads;
+        r.t = t;
+        r.window_K = c.window_K;
+        r.dur_len = ctx->dur_len;
+        r.history_W = c.history_W;
+        r.scope_token = a.scope_token;
+        r.first_layer = a.first_layer;
+        r.tau_H = a.tau_H;
+        HIP_OK(ctx, launch_weight_relevance(r, s));
+    }
 
     ctx->next_layer = layer + 1;
     ctx->last_stream = s;
@@ -682,7 +761,9 @@ asrkf_status asrkf_stats(asrkf_ctx* ctx, asrkf_stats_t* out) {
     st = check_overflow(ctx, true);
     if (st != ASRKF_OK) return st;
     const asrkf_config& c = ctx->cfg;
-    const size_t inst = (size_t)c.n_layers * c.batch;
+    const size_t inst = (size_t)ctx->state_layers * c.batch;
+    // with token scope one list serves every layer: count it once per layer
+    const int64_t per_list = ctx->token_scope ? c.n_layers : 1;
     unsigned long long cnt[kCounters];
     std::vector<int32_t> na(inst);
     HIP_OK(ctx, hipMemcpy(cnt, ctx->counters, sizeof cnt, hipMemcpyDeviceToHost));
@@ -693,12 +774,14 @@ asrkf_status asrkf_stats(asrkf_ctx* ctx, asrkf_stats_t* out) {
     for (int b = 0; b < c.batch; ++b) total += (int64_t)(ctx->plen_host[b] + ctx->t) * c.n_layers;
     if (ctx->lists_ready) {
         for (size_t i = 0; i < inst; ++i) { current += na[i]; active += na[i] - 1; }
+        current *= per_list;
+        active *= per_list;
     } else {
         active = total;
     }
     out->total_positions = total;
     out->active_positions = active;
-    out->attended_total = ctx->lists_ready ? (int64_t)cnt[0] - current : 0;
+    out->attended_total = ctx->lists_ready ? (int64_t)cnt[0] * per_list - current : 0;
     for (int i = 1; i < 4; ++i) out->recoveries[i] = (int64_t)cnt[i] + ctx->host_recoveries[i];
     out->rr_requests = (int64_t)cnt[5];
     out->attn_launches = ctx->attn_launches;
@@ -718,7 +801,7 @@ asrkf_status asrkf_stats_reset(asrkf_ctx* ctx) {
     st = collect_timing(ctx);
     if (st != ASRKF_OK) return st;
     const asrkf_config& c = ctx->cfg;
-    const size_t inst = (size_t)c.n_layers * c.batch;
+    const size_t inst = (size_t)ctx->state_layers * c.batch;
     std::vector<int32_t> na(inst);
     HIP_OK(ctx, hipMemcpy(na.data(), ctx->n_active, inst * 4, hipMemcpyDeviceToHost));
     // keep the lists of the coming step counted, drop everything before it
@@ -752,7 +835,8 @@ asrkf_status asrkf_get_state(asrkf_ctx* ctx, int32_t layer, int32_t seq, int32_t
     st = check_overflow(ctx, true);
     if (st != ASRKF_OK) return st;
     const int n = ctx->plen_host[seq] + ctx->t;
-    const size_t off = ((size_t)layer * c.batch + seq) * ctx->cap;
+    const size_t sidx = (size_t)(ctx->token_scope ? 0 : layer) * c.batch + seq;
+    const size_t off = sidx * ctx->cap;
     std::vector<int32_t> U(n > 0 ? n : 1);
     if (n > 0) HIP_OK(ctx, hipMemcpy(U.data(), ctx->unfreeze + off, (size_t)n * 4, hipMemcpyDeviceToHost));
     if (n_positions) *n_positions = n;
@@ -763,7 +847,7 @@ asrkf_status asrkf_get_state(asrkf_ctx* ctx, int32_t layer, int32_t seq, int32_t
     if (active || n_active) {
         int32_t na = 0;
         if (ctx->lists_ready) {
-            HIP_OK(ctx, hipMemcpy(&na, ctx->n_active + ((size_t)layer * c.batch + seq), 4,
+            HIP_OK(ctx, hipMemcpy(&na, ctx->n_active + sidx, 4,
                                   hipMemcpyDeviceToHost));
             if (active && na > 0)
                 HIP_OK(ctx, hipMemcpy(active, ctx->list + off, (size_t)na * 4, hipMemcpyDeviceToHost));

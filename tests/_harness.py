@@ -106,28 +106,93 @@ def oracle_levels(w, inp, seq, modes=None, with_logits=True):
     return levels, ent
 
 
-def run_oracle(w, inp, instances, modes=None, with_logits=True, steps=None, record=None):
-    """Per instance: list over steps of dict(out, frozen, timer, count, active_next)."""
+def _oracle_instance(w, inp, l, b, steps):
+    K, V = inp.prompt(l, b)
+    return oracle.Instance(K, V, w.window_K, w.tau, w.k_soft, capacity=w.prefill[b] + steps + 1,
+                           history_W=w.history_W, relevance_kind=w.relevance)
+
+
+def _oracle_global(w, inp, b, steps):
+    KV = [inp.prompt(l, b) for l in range(w.n_layers)]
+    return oracle.GlobalInstance([k for k, _ in KV], [v for _, v in KV], w.window_K, w.tau,
+                                 w.k_soft, capacity=w.prefill[b] + steps + 1,
+                                 history_W=w.history_W, relevance_kind=w.relevance)
+
+
+def _record(inst, t, out, rec):
+    timer, count, frozen = inst.state()
+    act = np.concatenate([np.nonzero(~frozen)[0], [inst.n]])
+    return dict(t=t, out=out, frozen=frozen, timer=timer, count=count, active_next=act,
+                scores=rec.scores, attended=rec.active)
+
+
+def run_oracle(w, inp, instances, modes=None, with_logits=True, steps=None, record=None,
+               on_scores=None):
+    """Per instance: list over steps of dict(out, frozen, timer, count, active_next).
+    on_scores(l_or_None, b, t, n, attended, scores) sees every step's relevance."""
     steps = w.steps if steps is None else steps
     res = {}
+    if w.scope == "token":
+        for b in sorted({b for _, b in instances}):
+            levels, _ = oracle_levels(w, inp, b, modes, with_logits)
+            inst = _oracle_global(w, inp, b, steps)
+            layers = [l for l, bb in instances if bb == b]
+            recs = {l: [] for l in layers}
+            for t in range(1, steps + 1):
+                kv = [inp.new_token(l, b, t) for l in range(w.n_layers)]
+                rec = inst.step([inp.q(l, b, t) for l in range(w.n_layers)],
+                                [k for k, _ in kv], [v for _, v in kv])
+                if on_scores is not None:
+                    on_scores(None, b, t, inst.n, rec.active, rec.scores)
+                if levels[t - 1]:
+                    inst.recover(levels[t - 1], w.wr_last_N)
+                if record is None or record(t):
+                    for l in layers:
+                        recs[l].append(_record(inst, t, rec.out[l], rec))
+            for l in layers:
+                res[(l, b)] = recs[l]
+        return res
     for (l, b) in instances:
         levels, _ = oracle_levels(w, inp, b, modes, with_logits)
-        K, V = inp.prompt(l, b)
-        inst = oracle.Instance(K, V, w.window_K, w.tau, w.k_soft,
-                               capacity=w.prefill[b] + steps + 1)
+        inst = _oracle_instance(w, inp, l, b, steps)
         recs = []
         for t in range(1, steps + 1):
             kn, vn = inp.new_token(l, b, t)
             rec = inst.step(inp.q(l, b, t), kn, vn)
+            if on_scores is not None:
+                on_scores(l, b, t, inst.n, rec.active, rec.scores)
             if levels[t - 1]:
                 inst.recover(levels[t - 1], w.wr_last_N)
             if record is None or record(t):
-                timer, count, frozen = inst.state()
-                act = np.concatenate([np.nonzero(~frozen)[0], [inst.n]])
-                recs.append(dict(t=t, out=rec.out, frozen=frozen, timer=timer, count=count,
-                                 active_next=act, scores=rec.scores, attended=rec.active))
+                recs.append(_record(inst, t, rec.out, rec))
         res[(l, b)] = recs
     return res
+
+
+def fix_margin_run(w, margin, relative=False, modes=None, with_logits=True, max_rounds=40):
+    """Re-draw keys until every score the oracle actually compares with tau
+    (scored tokens outside the window, in the run's own active sets) keeps
+    |s - tau| >= margin (times tau when relative).  With token scope a
+    token's keys are re-drawn in every layer.  Returns the attempts map."""
+    attempts = {}
+    instances = [(l, b) for l in range(w.n_layers) for b in range(w.batch)]
+    lim = margin * abs(w.tau) if relative else margin
+    for _ in range(max_rounds):
+        bad = set()
+
+        def on_scores(l, b, t, n, A, s):
+            near = (np.abs(s - w.tau) < lim) & (A < n - w.window_K)
+            for j in A[near]:
+                for ll in (range(w.n_layers) if l is None else [l]):
+                    bad.add((ll, b, int(j)))
+
+        run_oracle(w, Inputs(w, attempts), instances, modes, with_logits, on_scores=on_scores)
+        if not bad:
+            return attempts
+        for (l, b, j) in bad:
+            a = attempts.setdefault((l, b), np.zeros(w.prefill[b] + w.steps, dtype=np.int64))
+            a[j] += 1
+    raise RuntimeError("could not keep the scores away from tau")
 
 
 # --------------------------------------------------------------------------
@@ -154,7 +219,8 @@ def run_gpu(w, inp, instances, modes=None, with_logits=True, steps=None, record=
                         w.max_ctx, w.window_K, w.tau, w.k_soft, w.vocab,
                         entropy_spike=w.entropy_spike, conf_drop=w.conf_drop,
                         wr_last_N=w.wr_last_N, dtype=w.dtype, spill_min_D=w.spill_min_D,
-                        device_rows=w.device_rows)
+                        device_rows=w.device_rows, history_W=w.history_W,
+                        relevance=w.relevance, scope=w.scope)
     ctx = A.asrkf_init(cfg)
     res = {key: [] for key in instances}
     seqmon = {b: [] for b in range(w.batch)}
@@ -338,3 +404,17 @@ def compare_sampled(w, inp, instances, outs, states, record_steps):
                 gs["out"] = g
                 compare_instance([gs], [o], check_out=False)
     return worst
+
+
+def score_quantile_run(w, qtl, steps=8):
+    """The qtl quantile of the scores of out-of-window tokens over the first
+    steps of the workload with nothing frozen (tau below every score)."""
+    vals = []
+    wq = w.replace(tau=-1.0, steps=steps, flat_logit_steps=())
+
+    def on_scores(l, b, t, n, A, s):
+        vals.append(s[A < n - w.window_K])
+
+    instances = [(l, b) for l in range(w.n_layers) for b in range(w.batch)]
+    run_oracle(wq, Inputs(wq), instances, with_logits=False, on_scores=on_scores)
+    return float(np.quantile(np.concatenate(vals), qtl))
