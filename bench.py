@@ -31,6 +31,11 @@ def parse():
     ap.add_argument("--workload", choices=sorted(WORKLOADS), default="32layer")
     ap.add_argument("--cpu-seconds", type=float, default=15.0,
                     help="budget of the oracle sample (0 disables the cpu_baseline leg)")
+    ap.add_argument("--relevance", choices=["abs", "softmax"], default=None,
+                    help="relevance reading (default: the workload's, Eq. 2 |q.k|)")
+    ap.add_argument("--scope", choices=["layer", "token"], default=None,
+                    help="token-state scope (default: per layer and sequence)")
+    ap.add_argument("--history-W", type=int, default=None, help="detection-count window (0 = all)")
     ap.add_argument("--layers", type=int, default=0,
                     help="run only the first N layers of the workload (counter runs); 0 = all")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",
@@ -111,12 +116,16 @@ def main():
     w = getattr(gen, WORKLOADS[args.workload])(steps=W + K)
     if args.layers:
         w = w.replace(n_layers=min(args.layers, w.n_layers))
+    for key in ("relevance", "scope", "history_W"):
+        if getattr(args, key) is not None:
+            w = w.replace(**{key: getattr(args, key)})
     L, B, Hq, Hkv, D = w.n_layers, w.batch, w.n_q_heads, w.n_kv_heads, w.head_dim
     tdt = torch.bfloat16 if w.dtype == "bf16" else torch.float32
 
     cfg = A.make_config(L, B, Hq, Hkv, D, w.max_ctx, w.window_K, w.tau, w.k_soft, w.vocab,
                         entropy_spike=w.entropy_spike, conf_drop=w.conf_drop,
-                        wr_last_N=w.wr_last_N, dtype=w.dtype, spill_min_D=w.spill_min_D)
+                        wr_last_N=w.wr_last_N, dtype=w.dtype, spill_min_D=w.spill_min_D,
+                        history_W=w.history_W, relevance=w.relevance, scope=w.scope)
     ctx = A.asrkf_init(cfg)
     dg = DeviceGen(w)
     # prompt KV, one (layer, seq) at a time through a staging buffer
@@ -166,7 +175,9 @@ def main():
     algo_bytes = bytes_per_token * attended + 4 * w.vocab * B * K
     attn_s = st["attn_kernel_ms"] / 1e3
     achieved = bytes_per_token * attended / attn_s / 1e9
-    traffic = measured_traffic(w.name, K, W)
+    default_path = (w.relevance == "abs" and w.scope == "layer" and not w.history_W
+                    and not w.spill_min_D)
+    traffic = measured_traffic(w.name, K, W) if default_path else None
     traffic, traffic_layers = traffic if traffic else (None, None)
     if args.copy_calibration > 0:
         src = torch.empty(args.copy_calibration, dtype=torch.uint8, device="cuda")
@@ -191,7 +202,8 @@ def main():
         "config": {"workload": w.name, "layers": L, "batch": B, "context": w.prefill[0]
                    if len(set(w.prefill)) == 1 else "ragged", "q_heads": Hq, "kv_heads": Hkv,
                    "head_dim": D, "window_K": w.window_K, "tau": w.tau, "k": w.k_soft,
-                   "vocab": w.vocab, "mode": "spill" if w.spill_min_D else "resident"},
+                   "vocab": w.vocab, "mode": "spill" if w.spill_min_D else "resident",
+                   "relevance": w.relevance, "scope": w.scope, "history_W": w.history_W},
         "decode_steps_per_s": K / elapsed,
         "hbm_fraction_step": algo_bytes / elapsed / 1e9 / PEAK_HBM_GBS,
         "attended_fraction": attended / max(1, sum(p + t for p in w.prefill
