@@ -13,7 +13,9 @@
 // range is walked in tiles dealt round-robin to its waves (a static deal, so
 // every run sums in the same order).  The waves' softmax states are merged
 // through LDS once per sequence the range touches, giving one partial
-// (m, l, acc) of every query head at slot (workgroup + sequence).
+// (m, l, acc) of every query head at slot (workgroup + sequence): when all
+// eight states fit in LDS each wave folds them for a slice of the rows in
+// one round, otherwise a three-round tree folds pairs.
 //
 // Lane layout inside a wave: 8 slots x 8 lanes.  Slot s holds KV head
 // s % Hkv of token s / Hkv of the iteration (8 / Hkv tokens per iteration),
@@ -177,6 +179,12 @@ __device__ __forceinline__ void fold(SoftState<BF16, D, G>& a, const float* bm, 
     }
 }
 
+// All 8 wave states fit in LDS next to the other buffers: merge in one round.
+template <bool BF16, int D, int G>
+constexpr bool merge_one_round() {
+    return (size_t)kWaves * (2 * G + G * Row<BF16, D>::kPerLane) * 64 * 4 <= 148 * 1024;
+}
+
 template <bool BF16, int D, int G, int HKV>
 __global__ void __launch_bounds__(64 * kWaves)
 attention_kernel(AttnArgs a) {
@@ -187,6 +195,7 @@ attention_kernel(AttnArgs a) {
     constexpr int TPI = 8 / HKV;                 // tokens per iteration
     constexpr int TT = kUnroll * TPI;            // tokens per tile
     constexpr int NV = 2 * G + G * EL;           // floats of a lane's state
+    constexpr bool kOneRound = merge_one_round<BF16, D, G>();
 
     extern __shared__ int32_t lds[];
     int32_t* seq_off = lds;                                      // [B + 1]
@@ -407,6 +416,79 @@ attention_kernel(AttnArgs a) {
             __syncthreads();                       // LDS chunk buffers are reused next
         }
 
+        if constexpr (kOneRound) {
+            // merge the 8 wave states in one round: every wave stores its state,
+            // then each wave folds all 8 states for its own rows (fixed order)
+            __syncthreads();
+            {
+                float* dst = merge_lds + (size_t)wave * NV * 64 + lane;
+#pragma unroll
+                for (int h = 0; h < G; ++h) {
+                    dst[(2 * h) * 64] = st.m[h];
+                    dst[(2 * h + 1) * 64] = st.l[h];
+#pragma unroll
+                    for (int e = 0; e < EL; ++e) dst[(2 * G + h * EL + e) * 64] = st.acc[h][e];
+                }
+            }
+            __syncthreads();
+            constexpr int RPW = G * EL / kWaves;          // acc rows folded by each wave
+            const int row0 = wave * RPW;                  // first row, within head hh
+            const int hh = row0 / EL, e0 = row0 % EL;
+            float M = -INFINITY;
+            float ms[kWaves];
+#pragma unroll
+            for (int s2 = 0; s2 < kWaves; ++s2) {
+                ms[s2] = merge_lds[((size_t)s2 * NV + 2 * hh) * 64 + lane];
+                M = fmaxf(M, ms[s2]);
+            }
+            float Lf = 0.f, accf[RPW];
+#pragma unroll
+            for (int i = 0; i < RPW; ++i) accf[i] = 0.f;
+#pragma unroll
+            for (int s2 = 0; s2 < kWaves; ++s2) {
+                const float wgt = (ms[s2] == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(ms[s2] - M);
+                Lf = fmaf(wgt, merge_lds[((size_t)s2 * NV + 2 * hh + 1) * 64 + lane], Lf);
+#pragma unroll
+                for (int i = 0; i < RPW; ++i)
+                    accf[i] = fmaf(wgt, merge_lds[((size_t)s2 * NV + 2 * G + hh * EL + e0 + i) * 64 + lane], accf[i]);
+            }
+            // slots holding the same KV head (different tokens of an iteration)
+#pragma unroll
+            for (int mask = 8 * HKV; mask < 64; mask <<= 1) {
+                const float om = __shfl_xor(M, mask), ol = __shfl_xor(Lf, mask);
+                float oa[RPW];
+#pragma unroll
+                for (int i = 0; i < RPW; ++i) oa[i] = __shfl_xor(accf[i], mask);
+                // fixed order: the lower lane's state first
+                const bool up = (lane & mask) != 0;
+                const float m1 = up ? om : M, m2 = up ? M : om;
+                const float Mn = fmaxf(m1, m2);
+                const float w1 = (m1 == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(m1 - Mn);
+                const float w2 = (m2 == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(m2 - Mn);
+                const float l1 = up ? ol : Lf, l2 = up ? Lf : ol;
+                Lf = l1 * w1 + l2 * w2;
+#pragma unroll
+                for (int i = 0; i < RPW; ++i) {
+                    const float a1 = up ? oa[i] : accf[i], a2 = up ? accf[i] : oa[i];
+                    accf[i] = a1 * w1 + a2 * w2;
+                }
+                M = Mn;
+            }
+            __syncthreads();                       // merge buffer reads done: chunks may restage
+            if (tk == 0) {
+                const size_t part = (size_t)(w + b) * a.Hq + (size_t)g * G + hh;
+                float* dst = a.part_acc + part * D;
+#pragma unroll
+                for (int i = 0; i < RPW; ++i) {
+                    const int e = e0 + i;
+                    dst[(e / R::kPerChunk) * (128 / R::kElem) + r * R::kPerChunk + (e % R::kPerChunk)] = accf[i];
+                }
+                if (r == 0 && e0 == 0) {
+                    a.part_ml[part * 2 + 0] = M;
+                    a.part_ml[part * 2 + 1] = Lf;
+                }
+            }
+        } else {
         // merge the waves' states: a fixed tree through LDS (4 -> 2 -> 1 partners)
 #pragma unroll
         for (int half = kWaves / 2; half >= 1; half >>= 1) {
@@ -486,42 +568,31 @@ attention_kernel(AttnArgs a) {
                 }
             }
         }
+        }
         x = sb + i1;
     }
 }
 
 // Split combine.  A block owns 64 dims of one query head of one sequence;
-// its 4 slot groups each take every 4th partial slot and the groups' sums are
-// added in a fixed order:
+// its 4 slot groups each fold every 4th partial slot into a running
+// (max, sum, acc) in one pass (all loads of a group issued together), and
+// the groups' states are folded in a fixed order:
 //   out[b][h][d] = sum_s 2^(m_s - M) acc_s[d] / sum_s 2^(m_s - M) l_s.
 constexpr int kFinishThreads = 256;
 constexpr int kFinishDims = 64;
 constexpr int kSlotGroups = kFinishThreads / kFinishDims;
-constexpr int kSlotUnroll = 4;
+constexpr int kSlotUnroll = 8;
 
 __global__ void __launch_bounds__(kFinishThreads)
 finish_kernel(FinishArgs a, int D) {
-    __shared__ float red[kFinishThreads];
-    __shared__ float redl[kFinishThreads];
+    __shared__ float sm[kFinishThreads], sl[kFinishThreads], sa[kFinishThreads];
     const int per_head = D / kFinishDims;
     const int bh = blockIdx.x / per_head;                 // b * Hq + h
     const int d = (blockIdx.x % per_head) * kFinishDims + threadIdx.x % kFinishDims;
     const int grp = threadIdx.x / kFinishDims;
     const int b = bh / a.Hq, h = bh % a.Hq;
     const int s0 = a.slot_first[b], s1 = a.slot_end[b];
-    // M = max over the slots of m_s (every thread of the block takes part)
-    float M = -INFINITY;
-    for (int k = s0 + (int)threadIdx.x; k < s1; k += kFinishThreads)
-        M = fmaxf(M, a.part_ml[((size_t)k * a.Hq + h) * 2]);
-    red[threadIdx.x] = M;
-    __syncthreads();
-    for (int o = kFinishThreads / 2; o > 0; o >>= 1) {
-        if ((int)threadIdx.x < o) red[threadIdx.x] = fmaxf(red[threadIdx.x], red[threadIdx.x + o]);
-        __syncthreads();
-    }
-    M = red[0];
-    __syncthreads();
-    float L = 0.f, acc = 0.f;
+    float M = -INFINITY, L = 0.f, acc = 0.f;
     for (int k = s0 + grp; k < s1; k += kSlotGroups * kSlotUnroll) {
         float mk[kSlotUnroll], lk[kSlotUnroll], ak[kSlotUnroll];
 #pragma unroll
@@ -532,28 +603,42 @@ finish_kernel(FinishArgs a, int D) {
             lk[u] = a.part_ml[head * 2 + 1];
             ak[u] = a.part_acc[head * D + d];
         }
+        float Mn = M;
+#pragma unroll
+        for (int u = 0; u < kSlotUnroll; ++u)
+            if (k + u * kSlotGroups < s1) Mn = fmaxf(Mn, mk[u]);
+        const float sc = (M == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(M - Mn);
+        L *= sc;
+        acc *= sc;
 #pragma unroll
         for (int u = 0; u < kSlotUnroll; ++u) {
             if (k + u * kSlotGroups < s1) {
-                const float wgt = __builtin_amdgcn_exp2f(mk[u] - M);
+                const float wgt = __builtin_amdgcn_exp2f(mk[u] - Mn);
                 L = fmaf(wgt, lk[u], L);
                 acc = fmaf(wgt, ak[u], acc);
             }
         }
+        M = Mn;
     }
-    red[threadIdx.x] = acc;
-    redl[threadIdx.x] = L;
+    sm[threadIdx.x] = M;
+    sl[threadIdx.x] = L;
+    sa[threadIdx.x] = acc;
     __syncthreads();
     if (grp == 0) {
+        float Mt = -INFINITY;
+#pragma unroll
+        for (int k = 0; k < kSlotGroups; ++k) Mt = fmaxf(Mt, sm[k * kFinishDims + threadIdx.x]);
         float o = 0.f, lt = 0.f;
 #pragma unroll
         for (int k = 0; k < kSlotGroups; ++k) {
-            o += red[k * kFinishDims + threadIdx.x];
-            lt += redl[k * kFinishDims + threadIdx.x];
+            const float mk = sm[k * kFinishDims + threadIdx.x];
+            const float wgt = (mk == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(mk - Mt);
+            o = fmaf(wgt, sa[k * kFinishDims + threadIdx.x], o);
+            lt = fmaf(wgt, sl[k * kFinishDims + threadIdx.x], lt);
         }
         a.out[(size_t)bh * D + d] = o / lt;
         if (a.norm && threadIdx.x == 0 && blockIdx.x % per_head == 0) {
-            a.norm[(size_t)bh * 2] = M;
+            a.norm[(size_t)bh * 2] = Mt;
             a.norm[(size_t)bh * 2 + 1] = lt;
         }
     }
@@ -565,7 +650,8 @@ constexpr int state_floats() { return 2 * G + G * Row<BF16, D>::kPerLane; }
 template <bool BF16, int D, int G>
 size_t lds_bytes(const AttnArgs& a) {
     const size_t chunk = (size_t)kChunk * (4 + 4 + 1);
-    const size_t merge = (size_t)(kWaves / 2) * state_floats<BF16, D, G>() * 64 * 4;
+    const size_t merge = (size_t)(merge_one_round<BF16, D, G>() ? kWaves : kWaves / 2) *
+                         state_floats<BF16, D, G>() * 64 * 4;
     return (size_t)(((a.B + 1 + 3) & ~3) + kDurCache) * 4 + (chunk > merge ? chunk : merge);
 }
 
