@@ -6,7 +6,10 @@ plus the split combine, then entropy, recovery and the rebuild of every
 active list.  Inputs are synthetic (seeded generator, device twin) and sit in
 HBM before the timed region starts.
 
-Prints one JSON line.  value = attended (active) KV token-layers per second.
+Prints one JSON line.  value = attended (active) KV token-layers per second,
+from a timed loop without instrumentation; the attention kernel's duration for
+the roofline comes from a replay of the same steps in which every attention
+dispatch records HIP events.
 """
 import argparse
 import json
@@ -126,18 +129,7 @@ def main():
                         entropy_spike=w.entropy_spike, conf_drop=w.conf_drop,
                         wr_last_N=w.wr_last_N, dtype=w.dtype, spill_min_D=w.spill_min_D,
                         history_W=w.history_W, relevance=w.relevance, scope=w.scope)
-    ctx = A.asrkf_init(cfg)
     dg = DeviceGen(w)
-    # prompt KV, one (layer, seq) at a time through a staging buffer
-    Pmax = max(w.prefill)
-    stage_k = torch.empty(Pmax * Hkv * D, dtype=tdt, device="cuda")
-    stage_v = torch.empty_like(stage_k)
-    for l in range(L):
-        for b in range(B):
-            P = w.prefill[b]
-            dg.kv_rows(l, b, 0, P, stage_k, stage_v)
-            A.asrkf_prefill(ctx, l, b, stage_k, stage_v, P)
-    del stage_k, stage_v
     S = W + K
     Q = torch.empty((S, L, B, Hq, D), dtype=tdt, device="cuda")
     Kn = torch.empty((S, L, B, Hkv, D), dtype=tdt, device="cuda")
@@ -147,33 +139,54 @@ def main():
     dg.new_kv(1, S, Kn, Vn)
     dg.logits(1, S, LG)
     out = torch.empty((L, B, Hq, D), dtype=torch.float32, device="cuda")
-    torch.cuda.synchronize()
 
-    def step(t):
-        i = t - 1
+    def run_pass(timing):
+        """A fresh context: prompt, W warm-up steps, then K timed steps."""
+        ctx = A.asrkf_init(cfg)
+        Pmax = max(w.prefill)
+        stage_k = torch.empty(Pmax * Hkv * D, dtype=tdt, device="cuda")
+        stage_v = torch.empty_like(stage_k)
         for l in range(L):
-            A.asrkf_decode_step(ctx, l, Q[i, l], Kn[i, l], Vn[i, l], out[l])
-        A.asrkf_restore(ctx, LG[i], A.AUTO)
+            for b in range(B):
+                P = w.prefill[b]
+                dg.kv_rows(l, b, 0, P, stage_k, stage_v)
+                A.asrkf_prefill(ctx, l, b, stage_k, stage_v, P)
+        torch.cuda.synchronize()
+        del stage_k, stage_v
 
-    for t in range(1, W + 1):
-        step(t)
-    torch.cuda.synchronize()
-    A.asrkf_stats_reset(ctx)
-    A.asrkf_set_timing(ctx, True)
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    for t in range(W + 1, W + K + 1):
-        step(t)
-    torch.cuda.synchronize()
-    elapsed = time.perf_counter() - t0
-    st = A.asrkf_stats(ctx)
-    A.asrkf_destroy(ctx)
+        def step(t):
+            i = t - 1
+            for l in range(L):
+                A.asrkf_decode_step(ctx, l, Q[i, l], Kn[i, l], Vn[i, l], out[l])
+            A.asrkf_restore(ctx, LG[i], A.AUTO)
+
+        for t in range(1, W + 1):
+            step(t)
+        torch.cuda.synchronize()
+        A.asrkf_stats_reset(ctx)
+        A.asrkf_set_timing(ctx, timing)
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for t in range(W + 1, W + K + 1):
+            step(t)
+        torch.cuda.synchronize()
+        elapsed = time.perf_counter() - t0
+        st = A.asrkf_stats(ctx)
+        A.asrkf_destroy(ctx)
+        return elapsed, st
+
+    # The step rate comes from a pass without instrumentation; the attention
+    # kernel's duration from a replay of the same steps in which every
+    # attention dispatch records HIP events (those add a few us per launch).
+    elapsed, st = run_pass(False)
+    _, st_timed = run_pass(True)
+    assert st_timed["attended_total"] == st["attended_total"]
     del Q, Kn, Vn, LG, out
 
     attended = st["attended_total"]
     bytes_per_token = w.kv_bytes_per_token()          # K + V of one token, one layer
     algo_bytes = bytes_per_token * attended + 4 * w.vocab * B * K
-    attn_s = st["attn_kernel_ms"] / 1e3
+    attn_s = st_timed["attn_kernel_ms"] / 1e3
     achieved = bytes_per_token * attended / attn_s / 1e9
     default_path = (w.relevance == "abs" and w.scope == "layer" and not w.history_W
                     and not w.spill_min_D)
@@ -214,10 +227,12 @@ def main():
                      "traffic_run_layers": traffic_layers,
                      "kernel": "attention_kernel<bf16, D=128, G=4, Hkv=8>",
                      "algorithmic_unit": f"{bytes_per_token} B per attended token-layer (K + V rows)",
-                     "launches": st["attn_launches"],
-                     "avg_launch_us": 1e3 * st["attn_kernel_ms"] / max(1, st["attn_launches"]),
+                     "launches": st_timed["attn_launches"],
+                     "avg_launch_us": 1e3 * st_timed["attn_kernel_ms"] / max(1, st_timed["attn_launches"]),
                      "algorithmic_bytes_per_launch": bytes_per_token * attended
-                     / max(1, st["attn_launches"])},
+                     / max(1, st_timed["attn_launches"]),
+                     "timing": "HIP events recorded by each attention dispatch, in a replay "
+                               "of the same warm-up and timed steps"},
     }
     if w.spill_min_D:
         row = bytes_per_token // 2                      # one K or V row
