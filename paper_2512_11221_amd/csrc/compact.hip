@@ -125,10 +125,12 @@ compact_kernel(CompactArgs a) {
     const int tid = threadIdx.x;
     int listed = 0;
 
+    int u_next[4];
+    load4(U, 4 * tid, n, u_next, 0);
     for (int p0 = 0; p0 < n; p0 += 4 * kThreads) {
         const int p = p0 + 4 * tid;
-        int u[4];
-        load4(U, p, n, u, 0);
+        int u[4] = {u_next[0], u_next[1], u_next[2], u_next[3]};
+        if (p0 + 4 * kThreads < n) load4(U, p + 4 * kThreads, n, u_next, 0);   // next tile in flight
         bool flag[4];
         bool dirty = false;
         if (a.scope_token) {

@@ -1,8 +1,9 @@
 // Entropy of the next-token distribution and the recovery ladder (Sec. 3.6).
 //
 // kEntropySplit workgroups per sequence, one pass over the V logits.  Each
-// thread keeps (m, S, T) with S = sum e^(x-m) and T = sum e^(x-m) (x-m) over
-// its logits; the triples are merged across the block and stored.  The last
+// thread forms (m, S, T) with S = sum e^(x-m) and T = sum e^(x-m) (x-m) over
+// its logits (all loads of a round in flight together, the round's maximum
+// first); the triples are merged across the block and stored.  The last
 // block of a sequence to finish (a per-sequence ticket) merges the stored
 // triples in block order and forms
 //     H = ln S - T / S          (nats, softmax at temperature 1)
@@ -22,21 +23,6 @@ struct Triple {
     float m, S, T;
 };
 
-__device__ __forceinline__ void push(Triple& a, float x) {
-    if (x > a.m) {
-        const float d = a.m - x;              // <= 0 (or -inf when empty)
-        const float e = (a.S > 0.f) ? expf(d) : 0.f;
-        a.T = (a.S > 0.f) ? e * (a.T + d * a.S) : 0.f;
-        a.S = a.S * e + 1.f;
-        a.m = x;
-    } else {
-        const float d = x - a.m;
-        const float e = expf(d);
-        a.S += e;
-        a.T = fmaf(e, d, a.T);
-    }
-}
-
 __device__ __forceinline__ Triple merge(const Triple& a, const Triple& b) {
     if (b.S == 0.f) return a;
     if (a.S == 0.f) return b;
@@ -50,6 +36,27 @@ __device__ __forceinline__ Triple merge(const Triple& a, const Triple& b) {
     return r;
 }
 
+// (m, S, T) of a thread's logits: its maximum first, then one pass with
+// e = exp(x - m) (as exp2 of pre-scaled differences), no data-dependent branch.
+template <int N>
+__device__ __forceinline__ Triple triple_of(const float (&x)[N], const bool (&ok)[N]) {
+    constexpr float kLog2e = 1.4426950408889634f;
+    float m = -INFINITY;
+#pragma unroll
+    for (int i = 0; i < N; ++i) m = ok[i] ? fmaxf(m, x[i]) : m;
+    float S = 0.f, T = 0.f;
+#pragma unroll
+    for (int i = 0; i < N; ++i) {
+        const float d = x[i] - m;
+        const float e = ok[i] ? __builtin_amdgcn_exp2f(d * kLog2e) : 0.f;
+        S += e;
+        T = fmaf(e, ok[i] ? d : 0.f, T);
+    }
+    return Triple{m, S, T};
+}
+
+constexpr int kVec = 4;             // float4 loads per thread per round
+
 __global__ void __launch_bounds__(kThreads)
 entropy_kernel(EntropyArgs a) {
     __shared__ Triple part[kThreads / 64];
@@ -61,13 +68,29 @@ entropy_kernel(EntropyArgs a) {
     if (((reinterpret_cast<uintptr_t>(x) & 15) == 0) && (a.V % 4 == 0)) {
         const int n4 = a.V / 4;
         const int i0 = (int)((int64_t)sp * n4 / kEntropySplit), i1 = (int)((int64_t)(sp + 1) * n4 / kEntropySplit);
-        for (int i = i0 + threadIdx.x; i < i1; i += kThreads) {
-            const float4 f = reinterpret_cast<const float4*>(x)[i];
-            push(acc, f.x); push(acc, f.y); push(acc, f.z); push(acc, f.w);
+        // all of a round's loads are issued before any of them is used
+        for (int base = i0; base < i1; base += kThreads * kVec) {
+            float v[4 * kVec];
+            bool ok[4 * kVec];
+#pragma unroll
+            for (int u = 0; u < kVec; ++u) {
+                const int i = base + u * kThreads + threadIdx.x;
+                const bool in = i < i1;
+                typedef float f4 __attribute__((ext_vector_type(4)));
+                const f4 f = in ? __builtin_nontemporal_load(reinterpret_cast<const f4*>(x) + i)
+                                : f4{0.f, 0.f, 0.f, 0.f};
+                v[4 * u] = f.x; v[4 * u + 1] = f.y; v[4 * u + 2] = f.z; v[4 * u + 3] = f.w;
+                ok[4 * u] = ok[4 * u + 1] = ok[4 * u + 2] = ok[4 * u + 3] = in;
+            }
+            acc = merge(acc, triple_of(v, ok));
         }
     } else {
         const int i0 = (int)((int64_t)sp * a.V / kEntropySplit), i1 = (int)((int64_t)(sp + 1) * a.V / kEntropySplit);
-        for (int i = i0 + threadIdx.x; i < i1; i += kThreads) push(acc, x[i]);
+        for (int i = i0 + threadIdx.x; i < i1; i += kThreads) {
+            const float v[1] = {x[i]};
+            const bool ok[1] = {true};
+            acc = merge(acc, triple_of(v, ok));
+        }
     }
     for (int o = 32; o > 0; o >>= 1) {
         Triple other{__shfl_xor(acc.m, o), __shfl_xor(acc.S, o), __shfl_xor(acc.T, o)};
@@ -82,17 +105,23 @@ entropy_kernel(EntropyArgs a) {
         __hip_atomic_store(dst, r.m, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         __hip_atomic_store(dst + 1, r.S, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         __hip_atomic_store(dst + 2, r.T, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        __threadfence();
-        last = (atomicAdd(a.ticket + b, 1) == kEntropySplit - 1);
+        // the device-scope stores above have completed before the ticket is taken,
+        // so no cache-wide write-back is needed
+        __builtin_amdgcn_s_waitcnt(0);
+        last = (__hip_atomic_fetch_add(a.ticket + b, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)
+                == kEntropySplit - 1);
     }
     __syncthreads();
     if (!last || threadIdx.x != 0) return;
-    __threadfence();
-    // the other blocks' triples, read at device scope (they may sit in another XCD's L2)
+    // the other blocks' triples, read at device scope (they may sit in another XCD's L2),
+    // all loads issued before the fixed-order merge
     float* src = a.partial + (size_t)b * kEntropySplit * 3;
-    auto ld = [](float* p) { return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT); };
-    Triple r{ld(src), ld(src + 1), ld(src + 2)};
-    for (int k = 1; k < kEntropySplit; ++k) r = merge(r, Triple{ld(src + 3 * k), ld(src + 3 * k + 1), ld(src + 3 * k + 2)});
+    float tv[3 * kEntropySplit];
+#pragma unroll
+    for (int k = 0; k < 3 * kEntropySplit; ++k)
+        tv[k] = __hip_atomic_load(src + k, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    Triple r{tv[0], tv[1], tv[2]};
+    for (int k = 1; k < kEntropySplit; ++k) r = merge(r, Triple{tv[3 * k], tv[3 * k + 1], tv[3 * k + 2]});
     a.ticket[b] = 0;                           // ready for the next step
     const float H = logf(r.S) - r.T / r.S;
     const float pmax = 1.f / r.S;
