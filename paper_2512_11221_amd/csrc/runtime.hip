@@ -691,10 +691,10 @@ asrkf_status asrkf_restore(asrkf_ctx* ctx, const float* logits, asrkf_recover mo
     asrkf_status st = check_ctx(ctx);
     if (st != ASRKF_OK) return st;
     const asrkf_config& c = ctx->cfg;
+    if ((int)mode < ASRKF_AUTO || (int)mode > ASRKF_NONE) return fail(ASRKF_EINVAL, "unknown recovery mode");
     if (ctx->next_layer != c.n_layers)
         return fail(ASRKF_ESTATE, "restore before decode_step of every layer (next layer %d of %d)",
                     ctx->next_layer, c.n_layers);
-    if ((int)mode < ASRKF_AUTO || (int)mode > ASRKF_NONE) return fail(ASRKF_EINVAL, "unknown recovery mode");
     st = check_overflow(ctx, false);
     if (st != ASRKF_OK) return st;
     hipStream_t s = static_cast<hipStream_t>(stream);
