@@ -111,68 +111,132 @@ __device__ __forceinline__ void ballot4(const bool (&f)[4], int& before, int& mi
     }
 }
 
+// The rebuild of positions [lo, hi) of one instance.  MODE 0 applies the
+// step's updates (token-scope freeze loop, recovery) and writes the list;
+// MODE 1 applies the updates and only counts; MODE 2 writes the list from
+// the already updated U.  List entries start at list + out_base.  Returns
+// the number of listed positions (the same value in every thread).
+template <int MODE>
+__device__ int compact_range(const CompactArgs& a, const Ladder& r, size_t base, int n, int lo,
+                             int hi, int out_base, int* tot0, int* tot1) {
+    int32_t* U = a.unfreeze + base;
+    int32_t* list = a.list + base;
+    const int tid = threadIdx.x;
+    int listed = 0;
+    int u_next[4];
+    load4(U, lo + 4 * tid, hi, u_next, 0);
+    for (int p0 = lo; p0 < hi; p0 += 4 * kThreads) {
+        const int p = p0 + 4 * tid;
+        int u[4] = {u_next[0], u_next[1], u_next[2], u_next[3]};
+        if (p0 + 4 * kThreads < hi) load4(U, p + 4 * kThreads, hi, u_next, 0);   // next tile in flight
+        bool flag[4];
+        if constexpr (MODE != 2) {
+            bool dirty = false;
+            if (a.scope_token) {
+                // token scope: Algorithm 1's freeze loop for the whole sequence, on the
+                // relevance summed over every layer's heads (state before this step: U <= t attended)
+#pragma unroll
+                for (int k = 0; k < 4; ++k) {
+                    const int q = p + k;
+                    if (q < hi && u[k] <= a.t && q < n - a.window_K && a.rel_acc[base + q] < a.tau_LH) {
+                        const int c = detect(a.count, a.hmask, a.hlast, base + q, a.t, a.history_W);
+                        const int d = a.dur[min(c, a.dur_len - 1)];
+                        if (d >= 1) {
+                            u[k] = a.t + d;
+                            dirty = true;
+                        }
+                    }
+                }
+            }
+#pragma unroll
+            for (int k = 0; k < 4; ++k) {
+                bool hit;
+                const bool live = p + k < hi;
+                u[k] = recover(r, u[k], p + k, live, hit);
+                dirty |= hit;
+                flag[k] = live & (u[k] <= r.t1);
+            }
+            if (dirty) {
+                for (int k = 0; k < 4; ++k) if (p + k < hi) U[p + k] = u[k];
+            }
+        } else {
+#pragma unroll
+            for (int k = 0; k < 4; ++k) flag[k] = (p + k < hi) & (u[k] <= r.t1);
+        }
+        int before, mine;
+        ballot4(flag, before, mine);
+        const Scan sc = tile_scan(before, mine, 0, 0, tot0, tot1);
+        if constexpr (MODE != 1) {
+            int out = out_base + listed + sc.off0;
+#pragma unroll
+            for (int k = 0; k < 4; ++k) if (flag[k]) list[out++] = p + k;
+        }
+        listed += sc.tot0;
+    }
+    return listed;
+}
+
+// List tail of an instance: the position n that the next token will take.
+__device__ __forceinline__ void finish_list(const CompactArgs& a, int inst, size_t base, int n, int listed) {
+    a.list[base + listed] = n;
+    a.n_active[inst] = listed + 1;
+    atomicAdd(a.listed_total, (unsigned long long)(listed + 1));
+}
+
+// One workgroup per instance.
 __global__ void __launch_bounds__(kThreads)
 compact_kernel(CompactArgs a) {
     __shared__ int tot0[kWaves], tot1[kWaves];
-
     const int inst = blockIdx.x;
     const int b = inst % a.B;
     const int n = a.plen[b] + a.t;            // positions after step t
     const Ladder r = make_ladder(a, b, n);
     const size_t base = (size_t)inst * a.cap;
-    int32_t* U = a.unfreeze + base;
-    int32_t* list = a.list + base;
-    const int tid = threadIdx.x;
-    int listed = 0;
+    const int listed = compact_range<0>(a, r, base, n, 0, n, 0, tot0, tot1);
+    if (threadIdx.x == 0) finish_list(a, inst, base, n, listed);
+}
 
-    int u_next[4];
-    load4(U, 4 * tid, n, u_next, 0);
-    for (int p0 = 0; p0 < n; p0 += 4 * kThreads) {
-        const int p = p0 + 4 * tid;
-        int u[4] = {u_next[0], u_next[1], u_next[2], u_next[3]};
-        if (p0 + 4 * kThreads < n) load4(U, p + 4 * kThreads, n, u_next, 0);   // next tile in flight
-        bool flag[4];
-        bool dirty = false;
-        if (a.scope_token) {
-            // token scope: Algorithm 1's freeze loop for the whole sequence, on the
-            // relevance summed over every layer's heads (state before this step: U <= t attended)
-#pragma unroll
-            for (int k = 0; k < 4; ++k) {
-                const int q = p + k;
-                if (q < n && u[k] <= a.t && q < n - a.window_K && a.rel_acc[base + q] < a.tau_LH) {
-                    const int c = detect(a.count, a.hmask, a.hlast, base + q, a.t, a.history_W);
-                    const int d = a.dur[min(c, a.dur_len - 1)];
-                    if (d >= 1) {
-                        u[k] = a.t + d;
-                        dirty = true;
-                    }
-                }
-            }
-        }
-#pragma unroll
-        for (int k = 0; k < 4; ++k) {
-            bool hit;
-            const bool live = p + k < n;
-            u[k] = recover(r, u[k], p + k, live, hit);
-            dirty |= hit;
-            flag[k] = live & (u[k] <= r.t1);
-        }
-        if (dirty) {
-            for (int k = 0; k < 4; ++k) if (p + k < n) U[p + k] = u[k];
-        }
-        int before, mine;
-        ballot4(flag, before, mine);
-        const Scan sc = tile_scan(before, mine, 0, 0, tot0, tot1);
-        int out = listed + sc.off0;
-#pragma unroll
-        for (int k = 0; k < 4; ++k) if (flag[k]) list[out++] = p + k;
-        listed += sc.tot0;
+// Few, long instances: each instance is cut into segments of seg_len
+// positions, one workgroup each.  Pass A applies the updates and counts each
+// segment; pass B adds the counts of the segments before it and writes.
+__global__ void __launch_bounds__(kThreads)
+compact_count_kernel(CompactArgs a) {
+    __shared__ int tot0[kWaves], tot1[kWaves];
+    const int seg = blockIdx.x, inst = blockIdx.y;
+    const int b = inst % a.B;
+    const int n = a.plen[b] + a.t;
+    const int lo = seg * a.seg_len, hi = min(n, lo + a.seg_len);
+    int cnt = 0;
+    if (lo < hi) {
+        const Ladder r = make_ladder(a, b, n);
+        cnt = compact_range<1>(a, r, (size_t)inst * a.cap, n, lo, hi, 0, tot0, tot1);
     }
-    if (tid == 0) {
-        list[listed] = n;                     // the next token's position
-        a.n_active[inst] = listed + 1;
-        atomicAdd(a.listed_total, (unsigned long long)(listed + 1));
+    if (threadIdx.x == 0) a.seg_count[(size_t)inst * gridDim.x + seg] = cnt;
+}
+
+__global__ void __launch_bounds__(kThreads)
+compact_write_kernel(CompactArgs a) {
+    __shared__ int tot0[kWaves], tot1[kWaves];
+    __shared__ int prefix;
+    const int seg = blockIdx.x, inst = blockIdx.y;
+    const int b = inst % a.B;
+    const int n = a.plen[b] + a.t;
+    const int lo = seg * a.seg_len, hi = min(n, lo + a.seg_len);
+    const int last = n > 0 ? (n - 1) / a.seg_len : 0;
+    if (seg > last) return;
+    if (threadIdx.x == 0) {
+        int s = 0;
+        for (int k = 0; k < seg; ++k) s += a.seg_count[(size_t)inst * gridDim.x + k];
+        prefix = s;
     }
+    __syncthreads();
+    const size_t base = (size_t)inst * a.cap;
+    int cnt = 0;
+    if (lo < hi) {
+        const Ladder r = make_ladder(a, b, n);
+        cnt = compact_range<2>(a, r, base, n, lo, hi, prefix, tot0, tot1);
+    }
+    if (seg == last && threadIdx.x == 0) finish_list(a, inst, base, n, prefix + cnt);
 }
 
 __global__ void __launch_bounds__(kThreads)
@@ -331,11 +395,34 @@ spill_init_kernel(SpillInitArgs a) {
 }  // namespace
 
 hipError_t launch_compact(const CompactArgs& a, int n_instances, hipStream_t s) {
-    if (a.spill_min_D > 0)
+    if (a.spill_min_D > 0) {
         hipLaunchKernelGGL(compact_spill_kernel, dim3(n_instances), dim3(kThreads), 0, s, a);
-    else
+    } else if (a.n_seg <= 1) {
         hipLaunchKernelGGL(compact_kernel, dim3(n_instances), dim3(kThreads), 0, s, a);
+    } else {
+        const dim3 grid(a.n_seg, n_instances);
+        hipLaunchKernelGGL(compact_count_kernel, grid, dim3(kThreads), 0, s, a);
+        const hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return e;
+        hipLaunchKernelGGL(compact_write_kernel, grid, dim3(kThreads), 0, s, a);
+    }
     return hipGetLastError();
+}
+
+int compact_segments(int n_instances, int cap, int* seg_len) {
+    // enough workgroups to spread a few long instances over the device
+    constexpr int kTile = 4 * kThreads;
+    const int tiles = (cap + kTile - 1) / kTile;
+    if (n_instances >= 256) {                 // already one workgroup per CU: no second pass
+        *seg_len = cap;
+        return 1;
+    }
+    int n_seg = (512 + n_instances - 1) / n_instances;
+    if (n_seg > tiles) n_seg = tiles;
+    if (n_seg < 1) n_seg = 1;
+    const int per = (tiles + n_seg - 1) / n_seg;
+    *seg_len = per * kTile;
+    return (cap + *seg_len - 1) / *seg_len;
 }
 
 hipError_t launch_spill_init(const SpillInitArgs& a, int n_instances, hipStream_t s) {

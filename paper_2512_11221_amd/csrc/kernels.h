@@ -139,6 +139,9 @@ struct CompactArgs {
     int32_t* hlast;
     const int32_t* dur;
     int32_t dur_len, history_W, window_K;
+    // segmented rebuild of few, long instances (n_seg > 1)
+    int32_t n_seg, seg_len;
+    int32_t* seg_count;       // [instances][n_seg]
 };
 
 // First decode step in spill mode: prompt positions p < P sit in device rows
@@ -190,6 +193,8 @@ hipError_t attention_occupancy(const AttnArgs& a, int dtype_bf16, int head_dim, 
                                int* blocks_per_cu);
 hipError_t launch_finish(const FinishArgs& a, int head_dim, hipStream_t s);
 hipError_t launch_compact(const CompactArgs& a, int n_instances, hipStream_t s);
+// Segments per instance (and their length) for the rebuild; 1 = one workgroup per instance.
+int compact_segments(int n_instances, int cap, int* seg_len);
 hipError_t launch_weight_relevance(const RelevanceArgs& a, hipStream_t s);
 hipError_t launch_spill_init(const SpillInitArgs& a, int n_instances, hipStream_t s);
 hipError_t launch_xfer(const XferArgs& a, int n_instances, hipStream_t s);

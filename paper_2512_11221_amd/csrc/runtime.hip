@@ -113,6 +113,8 @@ struct asrkf_ctx {
     float* rel_acc = nullptr;     // [B][cap] (token scope)
     float* xlog = nullptr;        // [B][cap][Hq] (relevance by attention weight)
     float* norm = nullptr;        // [B][Hq][2]
+    int n_seg = 1, seg_len = 0;   // segmented list rebuild (few, long instances)
+    int32_t* seg_count = nullptr; // [state instances][n_seg]
 
     // spill mode
     bool spill = false;
@@ -195,7 +197,7 @@ void free_all(asrkf_ctx* ctx) {
                     ctx->counters, ctx->row_of, ctx->on_host, ctx->list_row, ctx->free_rows,
                     ctx->free_top, ctx->out_pos, ctx->out_row, ctx->n_out, ctx->in_pos, ctx->in_row,
                     ctx->n_in, ctx->overflow, ctx->hmask, ctx->hlast, ctx->rel_acc, ctx->xlog,
-                    ctx->norm};
+                    ctx->norm, ctx->seg_count};
     for (void* p : ptrs) if (p) (void)hipFree(p);
     void* host[] = {ctx->khost, ctx->vhost, ctx->overflow_host};
     for (void* p : host) if (p) (void)hipHostFree(p);
@@ -324,6 +326,8 @@ asrkf_status asrkf_init(const asrkf_config* cfg, asrkf_ctx** out) {
         ALLOC(hlast, st_pos * 4);
     }
     if (ctx->token_scope) ALLOC(rel_acc, (size_t)c.batch * ctx->cap * 4);
+    ctx->n_seg = compact_segments((int)st_inst, ctx->cap, &ctx->seg_len);
+    if (ctx->n_seg > 1) ALLOC(seg_count, st_inst * ctx->n_seg * 4);
     if (c.relevance == ASRKF_REL_SOFTMAX) {
         ALLOC(xlog, (size_t)c.batch * ctx->cap * c.n_q_heads * 4);
         ALLOC(norm, (size_t)c.batch * c.n_q_heads * 2 * 4);
@@ -472,6 +476,9 @@ asrkf_status build_lists(asrkf_ctx* ctx, int forced_level, hipStream_t s) {
     a.B = ctx->cfg.batch;
     a.cap = ctx->cap;
     a.wr_last_N = ctx->cfg.wr_last_N;
+    a.n_seg = ctx->n_seg;
+    a.seg_len = ctx->seg_len;
+    a.seg_count = ctx->seg_count;
     if (ctx->token_scope && ctx->t > 0) {    // the step's freeze loop (not before the first step)
         a.scope_token = 1;
         a.rel_acc = ctx->rel_acc;
