@@ -645,8 +645,10 @@ asrkf_status asrkf_decode_step(asrkf_ctx* ctx, int32_t layer, const void* q, con
             ev = ctx->ev_free.back();
             ctx->ev_free.pop_back();
         } else {
-            HIP_OK(ctx, hipEventCreate(&ev.first));
-            HIP_OK(ctx, hipEventCreate(&ev.second));
+            // timing only: no system-scope fence (no cache write-back or invalidate)
+            // when the events complete, so they do not perturb the work they measure
+            HIP_OK(ctx, hipEventCreateWithFlags(&ev.first, hipEventDisableSystemFence));
+            HIP_OK(ctx, hipEventCreateWithFlags(&ev.second, hipEventDisableSystemFence));
         }
     }
     HIP_OK(ctx, launch_attention(a, c.dtype == ASRKF_BF16, c.head_dim, ctx->group, ctx->grid, s,
