@@ -166,20 +166,35 @@ def main():
         A.asrkf_stats_reset(ctx)
         A.asrkf_set_timing(ctx, timing)
         torch.cuda.synchronize()
+        series = {"gpu_ms": [], "attended": []}
         t0 = time.perf_counter()
         for t in range(W + 1, W + K + 1):
-            step(t)
+            if timing:
+                # the replay also records the per-step series: GPU time and attended
+                # token-layers of every step (the freezing cohort moves in lockstep)
+                e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                e0.record()
+                step(t)
+                e1.record()
+                e1.synchronize()
+                series["gpu_ms"].append(round(e0.elapsed_time(e1), 4))
+                series["attended"].append(A.asrkf_stats(ctx)["attended_total"])
+            else:
+                step(t)
         torch.cuda.synchronize()
         elapsed = time.perf_counter() - t0
         st = A.asrkf_stats(ctx)
         A.asrkf_destroy(ctx)
-        return elapsed, st
+        if timing:
+            cum = series["attended"]
+            series["attended"] = [c - p for c, p in zip(cum, [0] + cum[:-1])]
+        return elapsed, st, series
 
     # The step rate comes from a pass without instrumentation; the attention
     # kernel's duration from a replay of the same steps in which every
     # attention dispatch records HIP events (those add a few us per launch).
-    elapsed, st = run_pass(False)
-    _, st_timed = run_pass(True)
+    elapsed, st, _ = run_pass(False)
+    _, st_timed, series = run_pass(True)
     assert st_timed["attended_total"] == st["attended_total"]
     del Q, Kn, Vn, LG, out
 
@@ -222,6 +237,7 @@ def main():
         "attended_fraction": attended / max(1, sum(p + t for p in w.prefill
                                                    for t in range(W + 1, W + K + 1)) * L),
         "compression_after_run": st["compression"],
+        "step_series": series,
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": PEAK_HBM_GBS, "unit": "GB/s",
                      "frac": achieved / PEAK_HBM_GBS, "traffic": traffic,
                      "traffic_run_layers": traffic_layers,
