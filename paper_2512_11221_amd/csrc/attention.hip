@@ -33,7 +33,7 @@ namespace {
 constexpr int kWaves = 8;           // waves per workgroup
 constexpr int kUnroll = 4;          // iterations per tile
 constexpr int kChunk = 2048;        // tokens per LDS chunk (positions, freeze flags)
-constexpr int kMinPerGroup = 64;    // fewest tokens worth a workgroup
+constexpr int kMinPerGroup = 32;    // fewest tokens worth a workgroup
 constexpr int kDurCache = 512;      // Eq. 3 durations cached in LDS
 // raw buffer descriptor word 3 for gfx9-class targets (32-bit data, no swizzle)
 constexpr int kBufferFlags = 0x00020000;
