@@ -377,6 +377,225 @@ compact_spill_kernel(CompactArgs a) {
     }
 }
 
+// Spill mode for few, long instances: the same two passes cut into segments,
+// as three launches (pass 1 must push every released row before pass 2 pops).
+//   S1  recovery, then per segment: released rows, rows to copy out, positions
+//       that need a row back, listed positions;
+//   S2  releases (pushes in position order after the counts of the segments
+//       before), out-list entries;
+//   S3  the list and the rows it needs (pops in position order), and the tail.
+struct SegCounts {
+    int spill, first, need, flag;
+};
+
+// seg_count holds, per instance, n_seg count records and one more whose first
+// field is the stack height at the start of the rebuild (the last segment of
+// S3 overwrites free_top while other segments may still read it).
+__device__ __forceinline__ SegCounts seg_prefix(const CompactArgs& a, int inst, int seg) {
+    const int4* c = reinterpret_cast<const int4*>(a.seg_count) + (size_t)inst * (a.n_seg + 1);
+    SegCounts s{0, 0, 0, 0};
+    for (int k = 0; k < seg; ++k) {
+        const int4 v = c[k];
+        s.spill += v.x; s.first += v.y; s.need += v.z; s.flag += v.w;
+    }
+    return s;
+}
+
+__global__ void __launch_bounds__(kThreads)
+spill_count_kernel(CompactArgs a) {
+    __shared__ int tot0[kWaves], tot1[kWaves];
+    const int seg = blockIdx.x, inst = blockIdx.y;
+    const int b = inst % a.B;
+    const int n = a.plen[b] + a.t;
+    const int lo = seg * a.seg_len, hi = min(n, lo + a.seg_len);
+    const Ladder r = make_ladder(a, b, n);
+    const size_t base = (size_t)inst * a.cap;
+    int32_t* U = a.unfreeze + base;
+    const int32_t* row_of = a.row_of + base;
+    const uint8_t* on_host = a.on_host + base;
+    int ns = 0, nf = 0, nn = 0, nl = 0;
+    for (int p0 = lo; p0 < hi; p0 += 4 * kThreads) {
+        const int p = p0 + 4 * threadIdx.x;
+        int u[4], row[4];
+        load4(U, p, hi, u, 0);
+        load4(row_of, p, hi, row, -1);
+        bool spill[4], first[4], need[4], flag[4];
+        bool dirty = false;
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+            bool hit;
+            const bool live = p + k < hi;
+            u[k] = recover(r, u[k], p + k, live, hit);
+            dirty |= hit;
+            spill[k] = live & (row[k] >= 0) & (u[k] > r.t1) & (u[k] - a.t >= a.spill_min_D);
+            const bool stored = live ? on_host[p + k] != 0 : true;
+            first[k] = spill[k] & !stored;
+            flag[k] = live & (u[k] <= r.t1);
+            need[k] = flag[k] & (row[k] < 0);
+        }
+        if (dirty) {
+            for (int k = 0; k < 4; ++k) if (p + k < hi) U[p + k] = u[k];
+        }
+        int b0, m0, b1, m1;
+        ballot4(spill, b0, m0);
+        ballot4(first, b1, m1);
+        const Scan s1 = tile_scan(b0, m0, b1, m1, tot0, tot1);
+        ballot4(need, b0, m0);
+        ballot4(flag, b1, m1);
+        const Scan s2 = tile_scan(b0, m0, b1, m1, tot0, tot1);
+        ns += s1.tot0; nf += s1.tot1; nn += s2.tot0; nl += s2.tot1;
+    }
+    if (threadIdx.x == 0) {
+        int4* rec = reinterpret_cast<int4*>(a.seg_count) + (size_t)inst * (a.n_seg + 1);
+        rec[seg] = make_int4(ns, nf, nn, nl);
+        if (seg == 0) rec[a.n_seg] = make_int4(a.free_top[inst], 0, 0, 0);
+    }
+}
+
+__global__ void __launch_bounds__(kThreads)
+spill_push_kernel(CompactArgs a) {
+    __shared__ int tot0[kWaves], tot1[kWaves];
+    __shared__ SegCounts pre;
+    const int seg = blockIdx.x, inst = blockIdx.y;
+    const int b = inst % a.B;
+    const int n = a.plen[b] + a.t;
+    const int lo = seg * a.seg_len, hi = min(n, lo + a.seg_len);
+    if (lo >= hi) return;
+    if (threadIdx.x == 0) pre = seg_prefix(a, inst, seg);
+    __syncthreads();
+    const Ladder r = make_ladder(a, b, n);
+    const size_t base = (size_t)inst * a.cap;
+    const int32_t* U = a.unfreeze + base;
+    int32_t* row_of = a.row_of + base;
+    uint8_t* on_host = a.on_host + base;
+    int32_t* stack = a.free_rows + (size_t)inst * a.pool_rows;
+    const int top0 = reinterpret_cast<const int4*>(a.seg_count)[(size_t)inst * (a.n_seg + 1) + a.n_seg].x;
+    int pushed = pre.spill, n_out = pre.first;
+    for (int p0 = lo; p0 < hi; p0 += 4 * kThreads) {
+        const int p = p0 + 4 * threadIdx.x;
+        int u[4], row[4];
+        load4(U, p, hi, u, 0);                // already recovered by S1
+        load4(row_of, p, hi, row, -1);
+        bool spill[4], first[4];
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+            const bool live = p + k < hi;
+            spill[k] = live & (row[k] >= 0) & (u[k] > r.t1) & (u[k] - a.t >= a.spill_min_D);
+            const bool stored = live ? on_host[p + k] != 0 : true;
+            first[k] = spill[k] & !stored;
+        }
+        int b0, m0, b1, m1;
+        ballot4(spill, b0, m0);
+        ballot4(first, b1, m1);
+        const Scan sc = tile_scan(b0, m0, b1, m1, tot0, tot1);
+        int ps = top0 + pushed + sc.off0, po = n_out + sc.off1;
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+            if (first[k]) {
+                a.out_pos[base + po] = p + k;
+                a.out_row[base + po] = row[k];
+                on_host[p + k] = 1;
+                ++po;
+            }
+            if (spill[k]) {
+                if (ps < a.pool_rows) stack[ps] = row[k];
+                row_of[p + k] = -1;
+                ++ps;
+            }
+        }
+        pushed += sc.tot0;
+        n_out += sc.tot1;
+    }
+}
+
+__global__ void __launch_bounds__(kThreads)
+spill_list_kernel(CompactArgs a) {
+    __shared__ int tot0[kWaves], tot1[kWaves];
+    __shared__ SegCounts pre, all;
+    const int seg = blockIdx.x, inst = blockIdx.y;
+    const int b = inst % a.B;
+    const int n = a.plen[b] + a.t;
+    const int lo = seg * a.seg_len, hi = min(n, lo + a.seg_len);
+    const int last = n > 0 ? (n - 1) / a.seg_len : 0;
+    if (seg > last) return;
+    if (threadIdx.x == 0) {
+        pre = seg_prefix(a, inst, seg);
+        all = seg_prefix(a, inst, a.n_seg);
+    }
+    __syncthreads();
+    const Ladder r = make_ladder(a, b, n);
+    const size_t base = (size_t)inst * a.cap;
+    const int32_t* U = a.unfreeze + base;
+    int32_t* row_of = a.row_of + base;
+    const int32_t* stack = a.free_rows + (size_t)inst * a.pool_rows;
+    const int top0 = reinterpret_cast<const int4*>(a.seg_count)[(size_t)inst * (a.n_seg + 1) + a.n_seg].x;
+    const int top = min(a.pool_rows, top0 + all.spill);
+    int listed = pre.flag, popped = pre.need;
+    bool short_of_rows = false;
+    for (int p0 = lo; p0 < hi; p0 += 4 * kThreads) {
+        const int p = p0 + 4 * threadIdx.x;
+        int u[4], row[4];
+        load4(U, p, hi, u, 0);
+        load4(row_of, p, hi, row, -1);
+        bool flag[4], need[4];
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+            flag[k] = (p + k < hi) & (u[k] <= r.t1);
+            need[k] = flag[k] & (row[k] < 0);
+        }
+        int b0, m0, b1, m1;
+        ballot4(flag, b0, m0);
+        ballot4(need, b1, m1);
+        const Scan sc = tile_scan(b0, m0, b1, m1, tot0, tot1);
+        int pl = listed + sc.off0, pn = popped + sc.off1;
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+            if (!flag[k]) continue;
+            int dev = row[k];
+            if (need[k]) {
+                const int idx = top - 1 - pn;
+                if (idx >= 0) {
+                    dev = stack[idx];
+                    row_of[p + k] = dev;
+                    a.in_pos[base + pn] = p + k;
+                    a.in_row[base + pn] = dev;
+                } else {
+                    dev = 0;                  // no row left: results are void, the host is told
+                    short_of_rows = true;
+                }
+                ++pn;
+            }
+            a.list[base + pl] = p + k;
+            a.list_row[base + pl] = dev;
+            ++pl;
+        }
+        listed += sc.tot0;
+        popped += sc.tot1;
+    }
+    if (short_of_rows) *a.overflow = 1;
+    if (seg == last && threadIdx.x == 0) {
+        const int idx = top - 1 - all.need;   // the next token's row
+        int dev = 0;
+        if (idx >= 0) {
+            dev = stack[idx];
+            row_of[n] = dev;
+        } else {
+            *a.overflow = 1;
+        }
+        a.list[base + all.flag] = n;
+        a.list_row[base + all.flag] = dev;
+        a.free_top[inst] = max(0, idx);
+        const int restored = min(all.need, top);
+        a.n_out[inst] = all.first;
+        a.n_in[inst] = restored;
+        a.n_active[inst] = all.flag + 1;
+        atomicAdd(a.listed_total, (unsigned long long)(all.flag + 1));
+        if (all.first) atomicAdd(a.xfer + 0, (unsigned long long)all.first);
+        if (restored) atomicAdd(a.xfer + 1, (unsigned long long)restored);
+        if (all.spill) atomicAdd(a.xfer + 2, (unsigned long long)all.spill);
+    }
+}
+
 __global__ void __launch_bounds__(256)
 spill_init_kernel(SpillInitArgs a) {
     const int inst = blockIdx.x;
@@ -395,7 +614,16 @@ spill_init_kernel(SpillInitArgs a) {
 }  // namespace
 
 hipError_t launch_compact(const CompactArgs& a, int n_instances, hipStream_t s) {
-    if (a.spill_min_D > 0) {
+    if (a.spill_min_D > 0 && a.n_seg > 1) {
+        const dim3 grid(a.n_seg, n_instances);
+        hipLaunchKernelGGL(spill_count_kernel, grid, dim3(kThreads), 0, s, a);
+        hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return e;
+        hipLaunchKernelGGL(spill_push_kernel, grid, dim3(kThreads), 0, s, a);
+        e = hipGetLastError();
+        if (e != hipSuccess) return e;
+        hipLaunchKernelGGL(spill_list_kernel, grid, dim3(kThreads), 0, s, a);
+    } else if (a.spill_min_D > 0) {
         hipLaunchKernelGGL(compact_spill_kernel, dim3(n_instances), dim3(kThreads), 0, s, a);
     } else if (a.n_seg <= 1) {
         hipLaunchKernelGGL(compact_kernel, dim3(n_instances), dim3(kThreads), 0, s, a);

@@ -141,7 +141,7 @@ struct CompactArgs {
     int32_t dur_len, history_W, window_K;
     // segmented rebuild of few, long instances (n_seg > 1)
     int32_t n_seg, seg_len;
-    int32_t* seg_count;       // [instances][n_seg]
+    int32_t* seg_count;       // [instances][n_seg] counts ([instances][n_seg + 1][4] in spill mode)
 };
 
 // First decode step in spill mode: prompt positions p < P sit in device rows

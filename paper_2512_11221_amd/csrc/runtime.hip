@@ -327,7 +327,7 @@ asrkf_status asrkf_init(const asrkf_config* cfg, asrkf_ctx** out) {
     }
     if (ctx->token_scope) ALLOC(rel_acc, (size_t)c.batch * ctx->cap * 4);
     ctx->n_seg = compact_segments((int)st_inst, ctx->cap, &ctx->seg_len);
-    if (ctx->n_seg > 1) ALLOC(seg_count, st_inst * ctx->n_seg * 4);
+    if (ctx->n_seg > 1) ALLOC(seg_count, st_inst * (ctx->n_seg + 1) * 16);   // spill mode: 4 counts per segment
     if (c.relevance == ASRKF_REL_SOFTMAX) {
         ALLOC(xlog, (size_t)c.batch * ctx->cap * c.n_q_heads * 4);
         ALLOC(norm, (size_t)c.batch * c.n_q_heads * 2 * 4);

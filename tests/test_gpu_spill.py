@@ -134,3 +134,20 @@ def test_llama8b_one_layer_spill():
     w = gen.llama8b_1layer(spill_min_D=2)
     g, o, mon, stats = _spill_parity(w, H.Inputs(w))
     assert stats[-1]["rows_to_host"] > 1000
+
+
+def test_too_few_device_rows_long_instance():
+    """A long instance (rebuilt in segments) that outgrows its device rows."""
+    import paper_2512_11221_amd as A
+    w = gen.llama8b_1layer(spill_min_D=2, steps=24, device_rows=8192 + 6)
+    with pytest.raises(A.AsrkfError) as e:
+        H.run_gpu(w, H.Inputs(w), [(0, 0)], record=lambda t: t % 4 == 0)
+    assert e.value.code == A._lib.ECAPACITY
+
+
+def test_tight_device_rows_long_instance():
+    """Device rows just enough for the largest resident set of a long instance."""
+    w = gen.llama8b_1layer(spill_min_D=2, steps=40)
+    peak = _resident_peak(w, H.Inputs(w))
+    assert peak < w.max_ctx, peak
+    _spill_parity(w.replace(device_rows=peak), H.Inputs(w))
