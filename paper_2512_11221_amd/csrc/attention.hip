@@ -34,7 +34,14 @@ constexpr int kWaves = 8;           // waves per workgroup
 constexpr int kUnroll = 4;          // iterations per tile
 constexpr int kChunk = 2048;        // tokens per LDS chunk (positions, freeze flags)
 constexpr int kMinPerGroup = 32;    // fewest tokens worth a workgroup
+// Each sequence a workgroup takes part in costs it a fixed set-up and merge
+// (list staging, q, the freeze loop, the wave-state merge, a partial), about
+// what streaming this many tokens takes; the planner charges it as virtual
+// tokens ahead of every non-empty list, so a workgroup whose range straddles
+// two sequences gets correspondingly fewer real tokens.
+constexpr int kSeqCost = 48;
 constexpr int kDurCache = 512;      // Eq. 3 durations cached in LDS
+constexpr int kStage = kChunk / (64 * kWaves);   // chunk entries per thread
 // raw buffer descriptor word 3 for gfx9-class targets (32-bit data, no swizzle)
 constexpr int kBufferFlags = 0x00020000;
 // cache policy of the K/V row loads: non-temporal.  Each row is read once per
@@ -121,25 +128,40 @@ __device__ __forceinline__ void lane_axpy(LaneAcc<BF16, D>& acc, float p, const 
     }
 }
 
-// Token offsets of every sequence in the concatenated active lists:
-// seq_off[b] = sum of n_active[b'] for b' < b, seq_off[B] = T.  Wave 0 scans.
+// Offsets of every sequence in the concatenated, cost-padded active lists:
+// sequence b owns [seq_off[b], seq_off[b+1]), whose first kSeqCost entries
+// are virtual (none for an empty list); seq_off[B] = T.  Wave 0 scans.
 __device__ void plan_ranges(const int32_t* n_active, int B, int32_t* seq_off) {
     const int tid = threadIdx.x;
     if (tid < 64) {
+        constexpr int kBatch = 8;                 // counts loaded together
         const int per = (B + 63) / 64;
         const int b0 = tid * per;
         const int b1 = min(B, b0 + per);
         int mine = 0;
-        for (int b = b0; b < b1; ++b) mine += n_active[b];
+        for (int bb = b0; bb < b1; bb += kBatch) {
+            int cost[kBatch];
+#pragma unroll
+            for (int k = 0; k < kBatch; ++k) {
+                const int n = bb + k < b1 ? n_active[bb + k] : 0;
+                cost[k] = n > 0 ? n + kSeqCost : 0;
+            }
+#pragma unroll
+            for (int k = 0; k < kBatch; ++k) {
+                if (bb + k < b1) seq_off[bb + k] = cost[k];      // kept here until the scan is done
+                mine += cost[k];
+            }
+        }
         int incl = mine;
         for (int o = 1; o < 64; o <<= 1) {
             const int y = __shfl_up(incl, o);
             if (tid >= o) incl += y;
         }
         int run = incl - mine;
-        for (int b = b0; b < b1; ++b) {
-            seq_off[b] = run;
-            run += n_active[b];
+        for (int bb = b0; bb < b1; ++bb) {
+            const int c = seq_off[bb];
+            seq_off[bb] = run;
+            run += c;
         }
         if (tid == 63) seq_off[B] = incl;
     }
@@ -196,24 +218,30 @@ attention_kernel(AttnArgs a) {
     constexpr int TT = kUnroll * TPI;            // tokens per tile
     constexpr int NV = 2 * G + G * EL;           // floats of a lane's state
     constexpr bool kOneRound = merge_one_round<BF16, D, G>();
+    static_assert(HKV * R::kBytes <= 64 * kWaves * 16, "the appended row takes one piece per thread");
 
     extern __shared__ int32_t lds[];
     int32_t* seq_off = lds;                                      // [B + 1]
     int32_t* dur_lds = lds + ((a.B + 1 + 3) & ~3);               // [kDurCache]
     int32_t* pos_lds = dur_lds + kDurCache;                      // [kChunk]
     int32_t* row_lds = pos_lds + kChunk;                         // [kChunk] (spill mode)
-    uint8_t* flag_lds = reinterpret_cast<uint8_t*>(row_lds + kChunk);   // [kChunk]
+    float* rel_lds = reinterpret_cast<float*>(row_lds + kChunk);   // [kChunk] (token scope)
+    uint8_t* flag_lds = reinterpret_cast<uint8_t*>(rel_lds + kChunk);   // [kChunk]
     // the wave-state merge runs after the chunk loop: it reuses the chunk buffers
     float* merge_lds = reinterpret_cast<float*>(pos_lds);        // [kWaves/2][NV][64]
 
-    for (int i = threadIdx.x; i < kDurCache; i += blockDim.x) dur_lds[i] = a.dur[min(i, a.dur_len - 1)];
+    // the duration table's load overlaps the planner's (one memory round trip for both)
+    static_assert(kDurCache == 64 * kWaves, "one duration per thread");
+    const int dur_mine = a.dur[min((int)threadIdx.x, a.dur_len - 1)];
     plan_ranges(a.n_active, a.B, seq_off);
+    dur_lds[threadIdx.x] = dur_mine;
     __syncthreads();
     const int T = wave_uniform(seq_off[a.B]);
     const int Gn = active_groups(T, gridDim.x);
     if (blockIdx.x == 0) {
         for (int b = threadIdx.x; b < a.B; b += blockDim.x) {
-            const int x0 = seq_off[b], x1 = seq_off[b + 1];
+            // the workgroups holding the list's first and last real tokens
+            const int x0 = seq_off[b] + kSeqCost, x1 = seq_off[b + 1];
             a.slot_first[b] = x1 > x0 ? group_of(x0, T, Gn) + b : 0;
             a.slot_end[b] = x1 > x0 ? group_of(x1 - 1, T, Gn) + b + 1 : 0;
         }
@@ -243,13 +271,12 @@ attention_kernel(AttnArgs a) {
     }
     while (x < x_end) {
         while (wave_uniform(seq_off[b + 1]) <= x) ++b;   // skip empty lists
-        const int sb = wave_uniform(seq_off[b]);
+        const int sb = wave_uniform(seq_off[b]) + kSeqCost;   // the list's first real token
         const int se = wave_uniform(seq_off[b + 1]);
+        if (x_end <= sb) break;                  // the range ends among the virtual tokens
         const int nb = se - sb;
-        const int i0 = x - sb;
+        const int i0 = max(x, sb) - sb;
         const int i1 = min(se, x_end) - sb;
-        const int n_pos = a.plen[b] + a.t;       // positions after the append
-        const int wedge = n_pos - a.window_K;    // positions < wedge are outside the window
         const size_t seq_row = (size_t)b * a.cap;
         const size_t seg = (size_t)b * a.pool_rows * row_stride;
         const int32_t* list_b = a.list + seq_row;
@@ -258,15 +285,6 @@ attention_kernel(AttnArgs a) {
         const bool rel_abs = a.rel_mode == 0;
         const bool scope_token = a.scope_token != 0;
 
-        uint4 qr[G][NC];
-        {
-            const char* qb = (const char*)a.q + ((size_t)b * a.Hq + (size_t)g * G) * R::kBytes;
-#pragma unroll
-            for (int h = 0; h < G; ++h)
-#pragma unroll
-                for (int c = 0; c < NC; ++c)
-                    qr[h][c] = *reinterpret_cast<const uint4*>(qb + h * R::kBytes + c * 128 + r * 16);
-        }
         S st;
 #pragma unroll
         for (int h = 0; h < G; ++h) {
@@ -283,22 +301,60 @@ attention_kernel(AttnArgs a) {
 
         for (int c0 = i0; c0 < i1; c0 += kChunk) {
             const int len = min(kChunk, i1 - c0);
-            if (c0 + len == nb) {
-                // this chunk ends with the new token: append its row to the cache first
-                const int new_row = spill ? lrow_b[nb - 1] : n_pos - 1;
-                const size_t dst = seg + (size_t)new_row * row_stride;
-                const size_t src = (size_t)b * row_stride;
-                for (int o = threadIdx.x * 16; o < row_stride; o += blockDim.x * 16) {
-                    *reinterpret_cast<uint4*>((char*)a.kpool_w + dst + o) =
-                        *reinterpret_cast<const uint4*>((const char*)a.knew + src + o);
-                    *reinterpret_cast<uint4*>((char*)a.vpool_w + dst + o) =
-                        *reinterpret_cast<const uint4*>((const char*)a.vnew + src + o);
+            // a chunk that ends with the new token appends its row to the cache
+            // (a token row is at most 8 heads x 128 x 4 bytes, one 16-byte piece
+            // per thread); its loads overlap the staging loads below
+            const int app_off = threadIdx.x * 16;
+            const bool append = c0 + len == nb && app_off < row_stride;
+            uint4 knew_piece, vnew_piece;
+            int spill_row = 0;
+            if (append) {
+                const size_t src = (size_t)b * row_stride + app_off;
+                knew_piece = *reinterpret_cast<const uint4*>((const char*)a.knew + src);
+                vnew_piece = *reinterpret_cast<const uint4*>((const char*)a.vnew + src);
+                if (spill) spill_row = lrow_b[nb - 1];
+            }
+            const int n_pos = a.plen[b] + a.t;       // positions after the append
+            const int wedge = n_pos - a.window_K;    // positions < wedge are outside the window
+            // stage the chunk's positions (and device rows): every load first, then the
+            // stores; the query rows are requested in between, so the chunk's set-up
+            // costs one memory round trip
+            uint4 qr[G][NC];
+            {
+                int sp[kStage], sr[kStage];
+#pragma unroll
+                for (int k = 0; k < kStage; ++k) {
+                    const int i = threadIdx.x + k * 64 * kWaves;
+                    if (i < len) {
+                        sp[k] = list_b[c0 + i];
+                        if (spill) sr[k] = lrow_b[c0 + i];
+                    }
+                }
+                const __amdgpu_buffer_rsrc_t rq = __builtin_amdgcn_make_buffer_rsrc(
+                    (void*)((const char*)a.q + (size_t)b * a.Hq * R::kBytes), (short)0, a.Hq * R::kBytes,
+                    kBufferFlags);
+                const int qo = g * G * R::kBytes + r * 16;
+#pragma unroll
+                for (int h = 0; h < G; ++h)
+#pragma unroll
+                    for (int c = 0; c < NC; ++c)
+                        qr[h][c] = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(
+                            rq, qo + h * R::kBytes + c * 128, 0, 0));
+#pragma unroll
+                for (int k = 0; k < kStage; ++k) {
+                    const int i = threadIdx.x + k * 64 * kWaves;
+                    if (i < len) {
+                        pos_lds[i] = sp[k];
+                        if (spill) row_lds[i] = sr[k];
+                        flag_lds[i] = 0;
+                    }
                 }
             }
-            for (int i = threadIdx.x; i < len; i += blockDim.x) {
-                pos_lds[i] = list_b[c0 + i];
-                if (spill) row_lds[i] = lrow_b[c0 + i];
-                flag_lds[i] = 0;
+            if (append) {
+                const int new_row = spill ? spill_row : n_pos - 1;
+                const size_t dst = seg + (size_t)new_row * row_stride + app_off;
+                *reinterpret_cast<uint4*>((char*)a.kpool_w + dst) = knew_piece;
+                *reinterpret_cast<uint4*>((char*)a.vpool_w + dst) = vnew_piece;
             }
             __threadfence_block();
             __syncthreads();
@@ -354,9 +410,7 @@ attention_kernel(AttnArgs a) {
                         if constexpr (HKV >= 8) rel += lane_xor<32>(rel);
                         if (valid[u] && g == 0 && r == 0) {
                             if (scope_token) {
-                                // summed over layers here, the freeze loop runs at the step's end
-                                float* ra = a.rel_acc + seq_row + pos[u];
-                                *ra = a.first_layer ? rel : *ra + rel;
+                                rel_lds[tb + u * TPI + tk] = rel;
                             } else if (pos[u] < wedge && rel < a.tau_H) {
                                 flag_lds[tb + u * TPI + tk] = 1;
                             }
@@ -405,13 +459,51 @@ attention_kernel(AttnArgs a) {
             }
             __syncthreads();
 
+            if (scope_token && rel_abs) {
+                // token scope sums the score over the layers; the freeze loop runs at the step's end
+                float prev[kStage];
+#pragma unroll
+                for (int k = 0; k < kStage; ++k) {
+                    const int i = threadIdx.x + k * 64 * kWaves;
+                    prev[k] = (i < len && !a.first_layer) ? a.rel_acc[seq_row + pos_lds[i]] : 0.f;
+                }
+#pragma unroll
+                for (int k = 0; k < kStage; ++k) {
+                    const int i = threadIdx.x + k * 64 * kWaves;
+                    if (i < len) a.rel_acc[seq_row + pos_lds[i]] = prev[k] + rel_lds[i];
+                }
+            }
             // freeze loop over the chunk's flagged tokens (Alg. 1; Eq. 3)
-            for (int i = threadIdx.x; i < len; i += blockDim.x) {
-                if (!flag_lds[i]) continue;
-                const size_t o = seq_row + pos_lds[i];
-                const int c = detect(a.count, a.hmask, a.hlast, o, a.t, a.history_W);
-                const int d = c < kDurCache ? dur_lds[c] : a.dur[min(c, a.dur_len - 1)];
-                if (d >= 1) a.unfreeze[o] = a.t + d;
+            if (a.history_W == 0) {
+                // cumulative count: every count load first, then the updates
+                // (an entry without a flag reads the sequence's first count and ignores it)
+                int p[kStage], cnt[kStage];
+                bool f[kStage];
+#pragma unroll
+                for (int k = 0; k < kStage; ++k) {
+                    const int i = threadIdx.x + k * 64 * kWaves;
+                    f[k] = i < len && flag_lds[i];
+                    p[k] = f[k] ? pos_lds[i] : 0;
+                }
+#pragma unroll
+                for (int k = 0; k < kStage; ++k) cnt[k] = a.count[seq_row + p[k]];
+#pragma unroll
+                for (int k = 0; k < kStage; ++k) {
+                    if (!f[k]) continue;
+                    const size_t o = seq_row + p[k];
+                    const int c = cnt[k] + 1;
+                    a.count[o] = c;
+                    const int d = c < kDurCache ? dur_lds[c] : a.dur[min(c, a.dur_len - 1)];
+                    if (d >= 1) a.unfreeze[o] = a.t + d;
+                }
+            } else {
+                for (int i = threadIdx.x; i < len; i += blockDim.x) {
+                    if (!flag_lds[i]) continue;
+                    const size_t o = seq_row + pos_lds[i];
+                    const int c = detect(a.count, a.hmask, a.hlast, o, a.t, a.history_W);
+                    const int d = c < kDurCache ? dur_lds[c] : a.dur[min(c, a.dur_len - 1)];
+                    if (d >= 1) a.unfreeze[o] = a.t + d;
+                }
             }
             __syncthreads();                       // LDS chunk buffers are reused next
         }
@@ -649,7 +741,7 @@ constexpr int state_floats() { return 2 * G + G * Row<BF16, D>::kPerLane; }
 
 template <bool BF16, int D, int G>
 size_t lds_bytes(const AttnArgs& a) {
-    const size_t chunk = (size_t)kChunk * (4 + 4 + 1);
+    const size_t chunk = (size_t)kChunk * (4 + 4 + 4 + 1);
     const size_t merge = (size_t)(merge_one_round<BF16, D, G>() ? kWaves : kWaves / 2) *
                          state_floats<BF16, D, G>() * 64 * 4;
     return (size_t)(((a.B + 1 + 3) & ~3) + kDurCache) * 4 + (chunk > merge ? chunk : merge);
