@@ -7,11 +7,13 @@
 //   Alg. 1 freeze loop: j outside the window with s_j < tau gets c_j += 1 and,
 //          when d = floor(sqrt(c_j)/k) >= 1, the unfreeze step U_j = t + d.
 //
-// Work decomposition.  The active lists of all sequences, concatenated, are
-// cut into equal contiguous token ranges, one per workgroup of a fixed grid,
-// computed on the device from the active counts.  Inside a workgroup the
-// range is walked in tiles dealt round-robin to its waves (a static deal, so
-// every run sums in the same order).  The waves' softmax states are merged
+// Work decomposition.  The active lists of all sequences, concatenated (each
+// preceded by a few virtual tokens that stand for the fixed cost of a
+// sequence), are cut into equal contiguous ranges, one per workgroup of a
+// fixed grid, computed on the device from the active counts.  Inside a
+// workgroup the range is walked in tiles dealt round-robin to its waves (a
+// static deal, so every run sums in the same order); a wave that falls behind
+// the others raises its issue priority until it has caught up.  The waves' softmax states are merged
 // through LDS once per sequence the range touches, giving one partial
 // (m, l, acc) of every query head at slot (workgroup + sequence): when all
 // eight states fit in LDS each wave folds them for a slice of the rows in
@@ -221,6 +223,7 @@ attention_kernel(AttnArgs a) {
     static_assert(HKV * R::kBytes <= 64 * kWaves * 16, "the appended row takes one piece per thread");
 
     extern __shared__ int32_t lds[];
+    __shared__ unsigned tile_lead;                               // most tiles any wave has finished
     int32_t* seq_off = lds;                                      // [B + 1]
     int32_t* dur_lds = lds + ((a.B + 1 + 3) & ~3);               // [kDurCache]
     int32_t* pos_lds = dur_lds + kDurCache;                      // [kChunk]
@@ -356,6 +359,7 @@ attention_kernel(AttnArgs a) {
                 *reinterpret_cast<uint4*>((char*)a.kpool_w + dst) = knew_piece;
                 *reinterpret_cast<uint4*>((char*)a.vpool_w + dst) = vnew_piece;
             }
+            if (threadIdx.x == 0) tile_lead = 0;
             __threadfence_block();
             __syncthreads();
 
@@ -456,7 +460,20 @@ attention_kernel(AttnArgs a) {
                         lane_axpy<BF16, D>(st.acc[h], pr, vr[u]);
                     }
                 }
+                // Pacing.  The tiles are dealt statically (every run sums in the same
+                // order), but when several waves can issue the hardware favours the
+                // older ones, and over a long range the younger waves fall behind by
+                // about a tenth.  A wave that has finished fewer tiles than the
+                // workgroup's leader issues at a raised priority until it catches up.
+                {
+                    const unsigned done = (unsigned)((tb - wave * TT) / (kWaves * TT) + 1);
+                    unsigned lead = 0;
+                    if (lane == 0) lead = atomicMax(&tile_lead, done);
+                    if (done < (unsigned)wave_uniform((int)lead)) __builtin_amdgcn_s_setprio(2);
+                    else __builtin_amdgcn_s_setprio(0);
+                }
             }
+            __builtin_amdgcn_s_setprio(0);
             __syncthreads();
 
             if (scope_token && rel_abs) {
