@@ -94,11 +94,16 @@ def cpu_baseline(w, budget_s):
         steps = t
         if spent >= budget_s:
             break
+    instances = w.n_layers * w.batch
     return {"value": attended / spent, "unit": "active KV token-layers/s", "cores": threads,
             "kind": "oracle",
             "sample": f"layer 0, sequence 0 of {w.name}: steps 1..{steps} "
                       f"({attended} attended token-layers in {spent:.1f} s); "
-                      f"the full step has {w.n_layers * w.batch} such instances"}
+                      f"the full step has {instances} such instances",
+            "cpu_count": os.cpu_count(),
+            "affinity": len(os.sched_getaffinity(0)) if hasattr(os, "sched_getaffinity") else None,
+            "ms_per_step_extrapolated": 1e3 * spent / steps * instances,
+            "extrapolation": f"the sample's mean time per step x {instances} instances"}
 
 
 def main():
