@@ -138,6 +138,20 @@ def test_ragged_heavy_hitters_multilayer():
     _parity(w, H.Inputs(w))
 
 
+def test_short_and_empty_lists_among_long_ones():
+    """Twelve sequences whose lists range from the new token alone to a few
+    thousand entries.  With so few tokens the launch cuts ranges of ~32
+    entries, so ranges end inside a sequence's virtual cost tokens, straddle
+    sequence boundaries, or hold only virtual tokens: every such plan must
+    still cover each real entry exactly once."""
+    w = gen.Workload(name="short-lists", seed=gen.SEED + 43, n_layers=2, batch=12, n_q_heads=32,
+                     n_kv_heads=8, head_dim=128, dtype="bf16",
+                     prefill=[0, 1, 2, 30, 47, 48, 49, 95, 500, 1500, 3, 64], steps=30,
+                     window_K=8, tau=math.inf, k_soft=1.0, vocab=64, logit_sigma=1.0,
+                     recipe="gauss")
+    _parity(w, H.Inputs(w))
+
+
 def test_bitwise_determinism():
     w, inp = _tiny_freezing()
     a, _, _ = H.run_gpu(w, inp, [(0, 0)])
