@@ -12,12 +12,13 @@
 // sequence), are cut into equal contiguous ranges, one per workgroup of a
 // fixed grid, computed on the device from the active counts.  Inside a
 // workgroup the range is walked in tiles dealt round-robin to its waves (a
-// static deal, so every run sums in the same order); a wave that falls behind
-// the others raises its issue priority until it has caught up.  The waves' softmax states are merged
-// through LDS once per sequence the range touches, giving one partial
-// (m, l, acc) of every query head at slot (workgroup + sequence): when all
-// eight states fit in LDS each wave folds them for a slice of the rows in
-// one round, otherwise a three-round tree folds pairs.
+// static deal, so every run sums in the same order); a wave that falls
+// behind the others raises its issue priority until it has caught up.  The
+// waves' softmax states are merged through LDS once per sequence the range
+// touches, giving one partial (m, l, acc) of every query head at slot
+// (workgroup + sequence): when all eight states fit in LDS each wave folds
+// them for a slice of the rows in one round, otherwise a three-round tree
+// folds pairs.
 //
 // Lane layout inside a wave: 8 slots x 8 lanes.  Slot s holds KV head
 // s % Hkv of token s / Hkv of the iteration (8 / Hkv tokens per iteration),
