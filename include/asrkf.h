@@ -203,6 +203,13 @@ asrkf_status asrkf_get_state(asrkf_ctx* ctx, int32_t layer, int32_t seq,
 asrkf_status asrkf_get_residency(asrkf_ctx* ctx, int32_t layer, int32_t seq,
                                  int32_t* n_positions, int32_t* device_row, uint8_t* on_host);
 
+/* Test hook for spill mode: before each step's row copies, the library's side
+ * stream first runs a kernel that waits `microseconds` (0 = off, the default).
+ * The attention of the next step must still read the restored rows, which
+ * shows that it waits for the copies rather than for time.  Host-side switch;
+ * EINVAL outside [0, 1e6]. */
+asrkf_status asrkf_debug_delay_side(asrkf_ctx* ctx, int32_t microseconds);
+
 /* Entropy monitor of one sequence after the last restore (Sec. 3.6):
  * entropy (nats), top probability, consecutive spike steps, level applied.
  * Host outputs, any may be NULL.  Waits for all queued work. */

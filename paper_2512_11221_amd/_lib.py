@@ -78,6 +78,7 @@ def load():
         "asrkf_stats": ([P, ctypes.POINTER(asrkf_stats_t)], I32),
         "asrkf_stats_reset": ([P], I32),
         "asrkf_set_timing": ([P, I32], I32),
+        "asrkf_debug_delay_side": ([P, I32], I32),
         "asrkf_get_state": ([P, I32, I32, P, P, P, P, P, P], I32),
         "asrkf_get_seq": ([P, I32, P, P, P, P], I32),
         "asrkf_get_residency": ([P, I32, I32, P, P, P], I32),
@@ -157,6 +158,10 @@ def asrkf_stats(ctx):
 
 def asrkf_stats_reset(ctx):
     _check(load().asrkf_stats_reset(ctx))
+
+
+def asrkf_debug_delay_side(ctx, microseconds):
+    _check(load().asrkf_debug_delay_side(ctx, int(microseconds)))
 
 
 def asrkf_set_timing(ctx, enable):

@@ -155,6 +155,7 @@ struct asrkf_ctx {
     double attn_ms_done = 0.0;
     int64_t attn_launches = 0;
     int64_t host_recoveries[4] = {0, 0, 0, 0};
+    int side_delay_us = 0;              // test hook: side stream waits before its copies
     int device = 0;
 };
 
@@ -521,6 +522,7 @@ asrkf_status build_lists(asrkf_ctx* ctx, int forced_level, hipStream_t s) {
     // attention launch waits for
     HIP_OK(ctx, hipEventRecord(ctx->ev_lists, s));
     HIP_OK(ctx, hipStreamWaitEvent(ctx->side, ctx->ev_lists, 0));
+    if (ctx->side_delay_us > 0) HIP_OK(ctx, launch_delay(ctx->side_delay_us, ctx->side));
     XferArgs x{};
     x.kpool = static_cast<char*>(ctx->kpool);
     x.vpool = static_cast<char*>(ctx->vpool);
@@ -821,6 +823,15 @@ asrkf_status asrkf_stats_reset(asrkf_ctx* ctx) {
     for (int i = 0; i < 4; ++i) ctx->host_recoveries[i] = 0;
     ctx->attn_ms_done = 0.0;
     ctx->attn_launches = 0;
+    return ASRKF_OK;
+}
+
+asrkf_status asrkf_debug_delay_side(asrkf_ctx* ctx, int32_t microseconds) {
+    asrkf_status st = check_ctx(ctx);
+    if (st != ASRKF_OK) return st;
+    if (microseconds < 0 || microseconds > 1000000)
+        return fail(ASRKF_EINVAL, "side-stream delay must be in [0, 1e6] us, got %d", microseconds);
+    ctx->side_delay_us = microseconds;
     return ASRKF_OK;
 }
 

@@ -45,7 +45,20 @@ xfer_kernel(XferArgs a) {
     }
 }
 
+// Test hook: one wave that waits, without touching memory, until the given
+// number of 100 MHz real-time ticks has passed.  It always ends.
+__global__ void __launch_bounds__(64) delay_kernel(uint64_t ticks) {
+    const uint64_t t0 = __builtin_amdgcn_s_memrealtime();
+    while (__builtin_amdgcn_s_memrealtime() - t0 < ticks) __builtin_amdgcn_s_sleep(100);
+}
+
 }  // namespace
+
+hipError_t launch_delay(int microseconds, hipStream_t s) {
+    if (microseconds <= 0) return hipSuccess;
+    hipLaunchKernelGGL(delay_kernel, dim3(1), dim3(64), 0, s, (uint64_t)microseconds * 100u);
+    return hipGetLastError();
+}
 
 hipError_t launch_xfer(const XferArgs& a, int n_instances, hipStream_t s) {
     if (n_instances < 1 || a.row_bytes % 16) return hipErrorInvalidValue;

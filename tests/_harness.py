@@ -208,7 +208,7 @@ def _dev(x, dtype):
 
 
 def run_gpu(w, inp, instances, modes=None, with_logits=True, steps=None, record=None,
-            timing=False):
+            timing=False, side_delay_us=0):
     """Run the library; per instance a list of dict(out, unfreeze, count, frozen,
     active_next) for the recorded steps; per sequence the entropy monitor."""
     import torch
@@ -222,6 +222,8 @@ def run_gpu(w, inp, instances, modes=None, with_logits=True, steps=None, record=
                         device_rows=w.device_rows, history_W=w.history_W,
                         relevance=w.relevance, scope=w.scope)
     ctx = A.asrkf_init(cfg)
+    if side_delay_us:
+        A.asrkf_debug_delay_side(ctx, side_delay_us)
     res = {key: [] for key in instances}
     seqmon = {b: [] for b in range(w.batch)}
     stats = []

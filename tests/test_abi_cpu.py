@@ -61,6 +61,7 @@ def test_init_rejects_invalid_config(bad):
 def test_null_context_is_einval():
     lib = A.load()
     assert lib.asrkf_set_timing(None, 1) == A._lib.EINVAL
+    assert lib.asrkf_debug_delay_side(None, 5) == A._lib.EINVAL
     assert lib.asrkf_restore(None, None, 0, None) == A._lib.EINVAL
     assert "null context" in A.asrkf_last_error()
     lib.asrkf_destroy(None)

@@ -29,9 +29,9 @@ def gpu():
     return torch
 
 
-def _spill_parity(w, inp, modes=None, with_logits=True):
+def _spill_parity(w, inp, modes=None, with_logits=True, side_delay_us=0):
     instances = [(l, b) for l in range(w.n_layers) for b in range(w.batch)]
-    g, mon, stats = H.run_gpu(w, inp, instances, modes, with_logits)
+    g, mon, stats = H.run_gpu(w, inp, instances, modes, with_logits, side_delay_us=side_delay_us)
     o = H.run_oracle(w, inp, instances, modes, with_logits)
     restores = 0
     for key in instances:
@@ -111,6 +111,20 @@ def test_gaussian_freezing_with_recovery(spill_min_D):
     inp = H.Inputs(w, H.fix_margin(w))
     g, o, mon, stats = _spill_parity(w, inp)
     assert stats[-1]["recoveries"][1:] == [3, 2, 1]
+
+
+def test_restores_wait_for_a_delayed_side_stream():
+    """The side stream that carries the row copies first idles 3 ms every step
+    (a test hook), far longer than a step's attention.  Results must not change:
+    the next step's attention waits on the copies' events, and the append into
+    a reused row waits for that row's copy to the host."""
+    import paper_2512_11221_amd as A
+    w0 = gen.tiny()
+    w = gen.tiny(tau=H.score_quantile(w0, 0.6), spill_min_D=2)
+    inp = H.Inputs(w, H.fix_margin(w))
+    g, o, mon, stats = _spill_parity(w, inp, modes={20: A.SR, 33: A.WR, 47: A.FR},
+                                     with_logits=False, side_delay_us=3000)
+    assert stats[-1]["rows_from_host"] > 0
 
 
 def test_forced_recovery_modes():
