@@ -78,7 +78,7 @@ typedef struct {
     float   entropy_spike;   /* theta_H in nats; +inf disables the entropy trigger */
     float   conf_drop;       /* theta_p on the top probability; <= 0 disables */
     int32_t wr_last_N;       /* Window Reset span in positions; <= 0 means 4 * window_K */
-    asrkf_dtype dtype;       /* storage type of q, k, v */
+    int32_t dtype;           /* storage type of q, k, v: an asrkf_dtype value */
     int32_t spill_min_D;     /* 0: resident mode, frozen KV stays in HBM and only leaves
                                 the active list.  >= 1: spill mode (Sec. 3.2, frozen KV
                                 moved off the GPU): a token frozen for d >= spill_min_D
@@ -157,9 +157,10 @@ asrkf_status asrkf_decode_step(asrkf_ctx* ctx, int32_t layer, const void* q,
  * the next step (Algorithm 1 timer loop; Sec. 3.5).
  *   logits: device, [batch][vocab] float32, or NULL (no entropy; AUTO then
  *           applies no recovery)
- *   mode:   see asrkf_recover; a forced level applies to every sequence.
+ *   mode:   an asrkf_recover value; a forced level applies to every sequence;
+ *           EINVAL for any other value.
  * Must follow decode_step of the last layer (else ESTATE).  Asynchronous. */
-asrkf_status asrkf_restore(asrkf_ctx* ctx, const float* logits, asrkf_recover mode,
+asrkf_status asrkf_restore(asrkf_ctx* ctx, const float* logits, int32_t mode,
                            void* stream);
 
 /* Counters of the context (Table 1 columns, attended tokens, recoveries).

@@ -11,7 +11,8 @@ import math
 import os
 
 HERE = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(HERE, "libasrkf.so")
+# ASRKF_LIBRARY selects another build of the same library (a sanitizer build)
+LIB_PATH = os.environ.get("ASRKF_LIBRARY") or os.path.join(HERE, "libasrkf.so")
 
 OK, EINVAL, ENOMEM, EHIP, ESTATE, ECAPACITY = 0, -1, -2, -3, -4, -5
 BF16, F32 = 0, 1

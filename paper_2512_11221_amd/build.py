@@ -38,5 +38,28 @@ def build():
     return compile_shared([os.path.join(CSRC, s) for s in SOURCES], LIB)
 
 
+def build_sanitized(kinds=("address", "undefined"), out=None):
+    """The same library with the host code (the runtime and the launch code)
+    built under clang sanitizers; the device code is compiled as usual.  An
+    AddressSanitizer build needs the sanitizer runtime preloaded into the host
+    process.  Returns the path of the library (default: libasrkf_<kinds>.so
+    next to libasrkf.so); load it through ASRKF_LIBRARY."""
+    extra = []
+    for k in kinds:
+        extra += ["-Xarch_host", f"-fsanitize={k}"]
+    extra += ["-Xarch_host", "-fno-omit-frame-pointer", "-Xarch_host", "-shared-libsan"]
+    import glob
+    rt_dirs = sorted(glob.glob("/opt/rocm/llvm/lib/clang/*/lib/linux"))
+    if rt_dirs:                                   # find the sanitizer runtimes at load time
+        extra += [f"-Wl,-rpath,{rt_dirs[-1]}"]
+    out = out or os.path.join(HERE, "libasrkf_" + "_".join(kinds) + ".so")
+    return compile_shared([os.path.join(CSRC, s) for s in SOURCES], out, extra=extra)
+
+
 if __name__ == "__main__":
-    print(build())
+    import sys
+    if len(sys.argv) > 1 and sys.argv[1] == "--sanitize":
+        print(build_sanitized(tuple(sys.argv[2].split(",")) if len(sys.argv) > 2
+                              else ("address", "undefined")))
+    else:
+        print(build())

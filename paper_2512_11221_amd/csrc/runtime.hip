@@ -698,7 +698,7 @@ asrkf_status asrkf_decode_step(asrkf_ctx* ctx, int32_t layer, const void* q, con
     return ASRKF_OK;
 }
 
-asrkf_status asrkf_restore(asrkf_ctx* ctx, const float* logits, asrkf_recover mode, void* stream) {
+asrkf_status asrkf_restore(asrkf_ctx* ctx, const float* logits, int32_t mode, void* stream) {
     asrkf_status st = check_ctx(ctx);
     if (st != ASRKF_OK) return st;
     const asrkf_config& c = ctx->cfg;
