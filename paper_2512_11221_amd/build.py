@@ -11,6 +11,8 @@ SOURCES = ["attention.hip", "relevance.hip", "compact.hip", "entropy.hip", "xfer
 ARCH = "gfx950"
 # no packed fp32 instructions anywhere in the device code
 DEVICE_FLAGS = ["-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"]
+# roctx ranges over the ABI calls (marker traces)
+LINK = ["-L/opt/rocm/lib", "-lrocprofiler-sdk-roctx", "-Wl,-rpath,/opt/rocm/lib"]
 
 
 def hipcc():
@@ -24,7 +26,7 @@ def compile_shared(sources, out, extra=(), cwd=None):
     fd, tmp = tempfile.mkstemp(suffix=".so", dir=os.path.dirname(out))
     os.close(fd)
     cmd = [hipcc(), f"--offload-arch={ARCH}", "-O3", "-std=c++17", "-fPIC", "-shared",
-           *DEVICE_FLAGS, *extra, *sources, "-o", tmp]
+           *DEVICE_FLAGS, *extra, *sources, *LINK, "-o", tmp]
     try:
         subprocess.run(cmd, check=True, cwd=cwd, stdout=subprocess.PIPE, stderr=subprocess.STDOUT)
     except subprocess.CalledProcessError as e:

@@ -24,6 +24,8 @@
 #include <utility>
 #include <vector>
 
+#include <rocprofiler-sdk-roctx/roctx.h>
+
 #include "../../include/asrkf.h"
 #include "kernels.h"
 
@@ -171,6 +173,15 @@ asrkf_status hip_fail(asrkf_ctx* ctx, hipError_t e, const char* what) {
         hipError_t e_ = (expr);                                        \
         if (e_ != hipSuccess) return hip_fail((ctx), e_, #expr);       \
     } while (0)
+
+// A roctx range over one host call of the ABI, so that a marker trace
+// (rocprofv3 --marker-trace) shows the step's phases next to its kernels.
+struct TraceRange {
+    explicit TraceRange(const char* name) { roctxRangePushA(name); }
+    ~TraceRange() { roctxRangePop(); }
+    TraceRange(const TraceRange&) = delete;
+    TraceRange& operator=(const TraceRange&) = delete;
+};
 
 asrkf_status check_ctx(asrkf_ctx* ctx) {
     if (!ctx) return fail(ASRKF_EINVAL, "null context");
@@ -572,6 +583,7 @@ asrkf_status check_overflow(asrkf_ctx* ctx, bool synced) {
 
 asrkf_status asrkf_decode_step(asrkf_ctx* ctx, int32_t layer, const void* q, const void* k_new,
                                const void* v_new, float* out, void* stream) {
+    TraceRange range("asrkf_decode_step");
     asrkf_status st = check_ctx(ctx);
     if (st != ASRKF_OK) return st;
     const asrkf_config& c = ctx->cfg;
@@ -699,6 +711,7 @@ asrkf_status asrkf_decode_step(asrkf_ctx* ctx, int32_t layer, const void* q, con
 }
 
 asrkf_status asrkf_restore(asrkf_ctx* ctx, const float* logits, int32_t mode, void* stream) {
+    TraceRange range("asrkf_restore");
     asrkf_status st = check_ctx(ctx);
     if (st != ASRKF_OK) return st;
     const asrkf_config& c = ctx->cfg;
