@@ -204,6 +204,11 @@ __device__ __forceinline__ void fold(SoftState<BF16, D, G>& a, const float* bm, 
     }
 }
 
+// Query heads per KV head above which a lane keeps only half of them (the
+// softmax state of eight heads does not fit in a wave's registers).
+template <int G>
+constexpr int split_of() { return G >= 8 ? 2 : 1; }
+
 // All 8 wave states fit in LDS next to the other buffers: merge in one round.
 template <bool BF16, int D, int G>
 constexpr bool merge_one_round() {
@@ -214,13 +219,25 @@ template <bool BF16, int D, int G, int HKV>
 __global__ void __launch_bounds__(64 * kWaves)
 attention_kernel(AttnArgs a) {
     using R = Row<BF16, D>;
-    using S = SoftState<BF16, D, G>;
+    // Wide query groups (G = 8) are split in halves of GS heads: a lane keeps the
+    // softmax state of GS query heads only, so it fits in registers.  A virtual
+    // KV head is a (KV head, half) pair, VH of them.  When a token has more
+    // virtual heads than a wave has slots, NWG waves share each token (wave
+    // part p takes virtual heads 8p .. 8p + 7) and the relevance of the parts is
+    // summed in LDS after the tiles.
+    constexpr int kSplit = split_of<G>();
+    constexpr int GS = G / kSplit;               // query heads per lane
+    constexpr int VH = HKV * kSplit;             // virtual KV heads
+    constexpr int NWG = VH > 8 ? VH / 8 : 1;     // waves sharing a token
+    constexpr int SV = VH > 8 ? 8 : VH;          // virtual heads of a token in one wave
+    constexpr int kGroups = kWaves / NWG;        // tiles are dealt to groups of NWG waves
+    using S = SoftState<BF16, D, GS>;
     constexpr int NC = R::kChunks;
     constexpr int EL = R::kPerLane;
-    constexpr int TPI = 8 / HKV;                 // tokens per iteration
+    constexpr int TPI = 8 / SV;                  // tokens per iteration
     constexpr int TT = kUnroll * TPI;            // tokens per tile
-    constexpr int NV = 2 * G + G * EL;           // floats of a lane's state
-    constexpr bool kOneRound = merge_one_round<BF16, D, G>();
+    constexpr int NV = 2 * GS + GS * EL;         // floats of a lane's state
+    constexpr bool kOneRound = merge_one_round<BF16, D, GS>();
     static_assert(HKV * R::kBytes <= 64 * kWaves * 16, "the appended row takes one piece per thread");
 
     extern __shared__ int32_t lds[];
@@ -229,8 +246,9 @@ attention_kernel(AttnArgs a) {
     int32_t* dur_lds = lds + ((a.B + 1 + 3) & ~3);               // [kDurCache]
     int32_t* pos_lds = dur_lds + kDurCache;                      // [kChunk]
     int32_t* row_lds = pos_lds + kChunk;                         // [kChunk] (spill mode)
-    float* rel_lds = reinterpret_cast<float*>(row_lds + kChunk);   // [kChunk] (token scope)
-    uint8_t* flag_lds = reinterpret_cast<uint8_t*>(rel_lds + kChunk);   // [kChunk]
+    float* rel_lds = reinterpret_cast<float*>(row_lds + kChunk);   // [kChunk][NWG] (token scope;
+                                                                 // the parts' sums when NWG > 1)
+    uint8_t* flag_lds = reinterpret_cast<uint8_t*>(rel_lds + 2 * kChunk);   // [kChunk]
     // the wave-state merge runs after the chunk loop: it reuses the chunk buffers
     float* merge_lds = reinterpret_cast<float*>(pos_lds);        // [kWaves/2][NV][64]
 
@@ -254,10 +272,14 @@ attention_kernel(AttnArgs a) {
     if (w >= Gn) return;
 
     const int wave = wave_uniform(threadIdx.x >> 6);
+    const int wpart = wave % NWG;                 // the wave's share of each token's heads
+    const int wgrp = wave / NWG;                  // the wave's tile group
     const int lane = threadIdx.x & 63;
     const int slot = lane >> 3;
-    const int tk = slot / HKV;                    // token of the iteration
-    const int g = slot % HKV;                     // KV head
+    const int tk = slot / SV;                     // token of the iteration
+    const int vh = wpart * SV + slot % SV;        // virtual KV head
+    const int g = vh / kSplit;                    // KV head
+    const int qh0 = g * G + (vh % kSplit) * GS;   // the lane's first query head
     const int r = lane & 7;
     const int row_stride = HKV * R::kBytes;       // bytes per token (all KV heads)
     const int lane_off = g * R::kBytes + r * 16;
@@ -291,7 +313,7 @@ attention_kernel(AttnArgs a) {
 
         S st;
 #pragma unroll
-        for (int h = 0; h < G; ++h) {
+        for (int h = 0; h < GS; ++h) {
             st.m[h] = -INFINITY;
             st.l[h] = 0.f;
 #pragma unroll
@@ -323,7 +345,7 @@ attention_kernel(AttnArgs a) {
             // stage the chunk's positions (and device rows): every load first, then the
             // stores; the query rows are requested in between, so the chunk's set-up
             // costs one memory round trip
-            uint4 qr[G][NC];
+            uint4 qr[GS][NC];
             {
                 int sp[kStage], sr[kStage];
 #pragma unroll
@@ -337,9 +359,9 @@ attention_kernel(AttnArgs a) {
                 const __amdgpu_buffer_rsrc_t rq = __builtin_amdgcn_make_buffer_rsrc(
                     (void*)((const char*)a.q + (size_t)b * a.Hq * R::kBytes), (short)0, a.Hq * R::kBytes,
                     kBufferFlags);
-                const int qo = g * G * R::kBytes + r * 16;
+                const int qo = qh0 * R::kBytes + r * 16;
 #pragma unroll
-                for (int h = 0; h < G; ++h)
+                for (int h = 0; h < GS; ++h)
 #pragma unroll
                     for (int c = 0; c < NC; ++c)
                         qr[h][c] = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(
@@ -364,7 +386,7 @@ attention_kernel(AttnArgs a) {
             __threadfence_block();
             __syncthreads();
 
-            for (int tb = wave * TT; tb < len; tb += kWaves * TT) {
+            for (int tb = wgrp * TT; tb < len; tb += kGroups * TT) {
                 uint4 kr[kUnroll][NC], vr[kUnroll][NC];
                 bool valid[kUnroll];
                 int pos[kUnroll];
@@ -384,24 +406,24 @@ attention_kernel(AttnArgs a) {
                         vr[u][c] = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(rv, vo + c * 128, so, kStreamPolicy));
                     }
                 }
-                float xs[kUnroll][G];
+                float xs[kUnroll][GS];
 #pragma unroll
                 for (int u = 0; u < kUnroll; ++u)
 #pragma unroll
-                    for (int h = 0; h < G; ++h) xs[u][h] = lane_dot<BF16, D>(kr[u], qr[h]);
+                    for (int h = 0; h < GS; ++h) xs[u][h] = lane_dot<BF16, D>(kr[u], qr[h]);
                 // 8-lane sums (every lane of a slot ends with the same bits)
 #pragma unroll
                 for (int u = 0; u < kUnroll; ++u)
 #pragma unroll
-                    for (int h = 0; h < G; ++h) xs[u][h] += dpp_mov<0xB1>(xs[u][h]);   // quad_perm [1,0,3,2]
+                    for (int h = 0; h < GS; ++h) xs[u][h] += dpp_mov<0xB1>(xs[u][h]);   // quad_perm [1,0,3,2]
 #pragma unroll
                 for (int u = 0; u < kUnroll; ++u)
 #pragma unroll
-                    for (int h = 0; h < G; ++h) xs[u][h] += dpp_mov<0x4E>(xs[u][h]);   // quad_perm [2,3,0,1]
+                    for (int h = 0; h < GS; ++h) xs[u][h] += dpp_mov<0x4E>(xs[u][h]);   // quad_perm [2,3,0,1]
 #pragma unroll
                 for (int u = 0; u < kUnroll; ++u)
 #pragma unroll
-                    for (int h = 0; h < G; ++h) xs[u][h] += dpp_mov<0x141>(xs[u][h]);  // row_half_mirror
+                    for (int h = 0; h < GS; ++h) xs[u][h] += dpp_mov<0x141>(xs[u][h]);  // row_half_mirror
 
                 // relevance (Eq. 2): sum over the slot's heads, then over the token's KV-head slots
                 if (rel_abs) {
@@ -409,12 +431,15 @@ attention_kernel(AttnArgs a) {
                     for (int u = 0; u < kUnroll; ++u) {
                         float rel = 0.f;
 #pragma unroll
-                        for (int h = 0; h < G; ++h) rel += fabsf(xs[u][h]);
-                        if constexpr (HKV >= 2) rel += lane_xor<8>(rel);
-                        if constexpr (HKV >= 4) rel += lane_xor<16>(rel);
-                        if constexpr (HKV >= 8) rel += lane_xor<32>(rel);
-                        if (valid[u] && g == 0 && r == 0) {
-                            if (scope_token) {
+                        for (int h = 0; h < GS; ++h) rel += fabsf(xs[u][h]);
+                        if constexpr (SV >= 2) rel += lane_xor<8>(rel);
+                        if constexpr (SV >= 4) rel += lane_xor<16>(rel);
+                        if constexpr (SV >= 8) rel += lane_xor<32>(rel);
+                        if (valid[u] && slot % SV == 0 && r == 0) {
+                            if (NWG > 1) {
+                                // this wave's part of the sum: the parts meet after the tiles
+                                rel_lds[(tb + u * TPI + tk) * NWG + wpart] = rel;
+                            } else if (scope_token) {
                                 rel_lds[tb + u * TPI + tk] = rel;
                             } else if (pos[u] < wedge && rel < a.tau_H) {
                                 flag_lds[tb + u * TPI + tk] = 1;
@@ -423,24 +448,24 @@ attention_kernel(AttnArgs a) {
                     }
                 }
 
-                float y[kUnroll][G];
+                float y[kUnroll][GS];
 #pragma unroll
                 for (int u = 0; u < kUnroll; ++u)
 #pragma unroll
-                    for (int h = 0; h < G; ++h) y[u][h] = valid[u] ? xs[u][h] * a.scale_log2 : -INFINITY;
+                    for (int h = 0; h < GS; ++h) y[u][h] = valid[u] ? xs[u][h] * a.scale_log2 : -INFINITY;
                 if (!rel_abs) {
                     // relevance by attention weight needs the sequence's normaliser: keep the logits
 #pragma unroll
                     for (int u = 0; u < kUnroll; ++u) {
                         if (valid[u] && r == 0) {
-                            float* xl = a.xlog + (seq_row + c0 + tb + u * TPI + tk) * a.Hq + g * G;
+                            float* xl = a.xlog + (seq_row + c0 + tb + u * TPI + tk) * a.Hq + qh0;
 #pragma unroll
-                            for (int h = 0; h < G; ++h) xl[h] = y[u][h];
+                            for (int h = 0; h < GS; ++h) xl[h] = y[u][h];
                         }
                     }
                 }
 #pragma unroll
-                for (int h = 0; h < G; ++h) {
+                for (int h = 0; h < GS; ++h) {
                     float mt = st.m[h];
 #pragma unroll
                     for (int u = 0; u < kUnroll; ++u) mt = fmaxf(mt, y[u][h]);
@@ -455,7 +480,7 @@ attention_kernel(AttnArgs a) {
 #pragma unroll
                 for (int u = 0; u < kUnroll; ++u) {
 #pragma unroll
-                    for (int h = 0; h < G; ++h) {
+                    for (int h = 0; h < GS; ++h) {
                         const float pr = valid[u] ? __builtin_amdgcn_exp2f(y[u][h] - st.m[h]) : 0.f;
                         st.l[h] += pr;
                         lane_axpy<BF16, D>(st.acc[h], pr, vr[u]);
@@ -467,7 +492,7 @@ attention_kernel(AttnArgs a) {
                 // about a tenth.  A wave that has finished fewer tiles than the
                 // workgroup's leader issues at a raised priority until it catches up.
                 {
-                    const unsigned done = (unsigned)((tb - wave * TT) / (kWaves * TT) + 1);
+                    const unsigned done = (unsigned)((tb - wgrp * TT) / (kGroups * TT) + 1);
                     unsigned lead = 0;
                     if (lane == 0) lead = atomicMax(&tile_lead, done);
                     if (done < (unsigned)wave_uniform((int)lead)) __builtin_amdgcn_s_setprio(2);
@@ -477,6 +502,21 @@ attention_kernel(AttnArgs a) {
             __builtin_amdgcn_s_setprio(0);
             __syncthreads();
 
+            if constexpr (NWG > 1) {
+                // the token's score is the sum of its parts (fixed order); in layer
+                // scope it decides the flag here, in token scope the sum is kept below
+#pragma unroll
+                for (int k = 0; k < kStage; ++k) {
+                    const int i = threadIdx.x + k * 64 * kWaves;
+                    if (i < len) {
+                        float sum = 0.f;
+#pragma unroll
+                        for (int p2 = 0; p2 < NWG; ++p2) sum += rel_lds[i * NWG + p2];
+                        if (scope_token) rel_lds[i * NWG] = sum;
+                        else flag_lds[i] = rel_abs && pos_lds[i] < wedge && sum < a.tau_H;
+                    }
+                }
+            }
             if (scope_token && rel_abs) {
                 // token scope sums the score over the layers; the freeze loop runs at the step's end
                 float prev[kStage];
@@ -488,7 +528,7 @@ attention_kernel(AttnArgs a) {
 #pragma unroll
                 for (int k = 0; k < kStage; ++k) {
                     const int i = threadIdx.x + k * 64 * kWaves;
-                    if (i < len) a.rel_acc[seq_row + pos_lds[i]] = prev[k] + rel_lds[i];
+                    if (i < len) a.rel_acc[seq_row + pos_lds[i]] = prev[k] + rel_lds[i * NWG];
                 }
             }
             // freeze loop over the chunk's flagged tokens (Alg. 1; Eq. 3)
@@ -527,44 +567,49 @@ attention_kernel(AttnArgs a) {
         }
 
         if constexpr (kOneRound) {
-            // merge the 8 wave states in one round: every wave stores its state,
-            // then each wave folds all 8 states for its own rows (fixed order)
+            // merge the wave states in one round: every wave stores its state, then
+            // each wave folds the states of its part's waves for its own rows
+            // (fixed order)
             __syncthreads();
             {
                 float* dst = merge_lds + (size_t)wave * NV * 64 + lane;
 #pragma unroll
-                for (int h = 0; h < G; ++h) {
+                for (int h = 0; h < GS; ++h) {
                     dst[(2 * h) * 64] = st.m[h];
                     dst[(2 * h + 1) * 64] = st.l[h];
 #pragma unroll
-                    for (int e = 0; e < EL; ++e) dst[(2 * G + h * EL + e) * 64] = st.acc[h][e];
+                    for (int e = 0; e < EL; ++e) dst[(2 * GS + h * EL + e) * 64] = st.acc[h][e];
                 }
             }
             __syncthreads();
-            constexpr int RPW = G * EL / kWaves;          // acc rows folded by each wave
-            const int row0 = wave * RPW;                  // first row, within head hh
+            // the states of the waves of one part cover the same heads: fold those
+            constexpr int kPerPart = kWaves / NWG;
+            constexpr int RPW = GS * EL / kPerPart;       // acc rows folded by each wave
+            const int row0 = wgrp * RPW;                  // first row, within head hh
             const int hh = row0 / EL, e0 = row0 % EL;
             float M = -INFINITY;
-            float ms[kWaves];
+            float ms[kPerPart];
 #pragma unroll
-            for (int s2 = 0; s2 < kWaves; ++s2) {
-                ms[s2] = merge_lds[((size_t)s2 * NV + 2 * hh) * 64 + lane];
-                M = fmaxf(M, ms[s2]);
+            for (int j = 0; j < kPerPart; ++j) {
+                const int s2 = j * NWG + wpart;           // the part's waves, in order
+                ms[j] = merge_lds[((size_t)s2 * NV + 2 * hh) * 64 + lane];
+                M = fmaxf(M, ms[j]);
             }
             float Lf = 0.f, accf[RPW];
 #pragma unroll
             for (int i = 0; i < RPW; ++i) accf[i] = 0.f;
 #pragma unroll
-            for (int s2 = 0; s2 < kWaves; ++s2) {
-                const float wgt = (ms[s2] == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(ms[s2] - M);
+            for (int j = 0; j < kPerPart; ++j) {
+                const int s2 = j * NWG + wpart;
+                const float wgt = (ms[j] == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(ms[j] - M);
                 Lf = fmaf(wgt, merge_lds[((size_t)s2 * NV + 2 * hh + 1) * 64 + lane], Lf);
 #pragma unroll
                 for (int i = 0; i < RPW; ++i)
-                    accf[i] = fmaf(wgt, merge_lds[((size_t)s2 * NV + 2 * G + hh * EL + e0 + i) * 64 + lane], accf[i]);
+                    accf[i] = fmaf(wgt, merge_lds[((size_t)s2 * NV + 2 * GS + hh * EL + e0 + i) * 64 + lane], accf[i]);
             }
             // slots holding the same KV head (different tokens of an iteration)
 #pragma unroll
-            for (int mask = 8 * HKV; mask < 64; mask <<= 1) {
+            for (int mask = 8 * SV; mask < 64; mask <<= 1) {
                 const float om = __shfl_xor(M, mask), ol = __shfl_xor(Lf, mask);
                 float oa[RPW];
 #pragma unroll
@@ -586,7 +631,7 @@ attention_kernel(AttnArgs a) {
             }
             __syncthreads();                       // merge buffer reads done: chunks may restage
             if (tk == 0) {
-                const size_t part = (size_t)(w + b) * a.Hq + (size_t)g * G + hh;
+                const size_t part = (size_t)(w + b) * a.Hq + (size_t)qh0 + hh;
                 float* dst = a.part_acc + part * D;
 #pragma unroll
                 for (int i = 0; i < RPW; ++i) {
@@ -601,40 +646,40 @@ attention_kernel(AttnArgs a) {
         } else {
         // merge the waves' states: a fixed tree through LDS (4 -> 2 -> 1 partners)
 #pragma unroll
-        for (int half = kWaves / 2; half >= 1; half >>= 1) {
+        for (int half = kWaves / 2; half >= NWG; half >>= 1) {
             __syncthreads();
             if (wave >= half && wave < 2 * half) {
                 float* dst = merge_lds + (size_t)(wave - half) * NV * 64 + lane;
 #pragma unroll
-                for (int h = 0; h < G; ++h) {
+                for (int h = 0; h < GS; ++h) {
                     dst[(2 * h) * 64] = st.m[h];
                     dst[(2 * h + 1) * 64] = st.l[h];
 #pragma unroll
-                    for (int e = 0; e < EL; ++e) dst[(2 * G + h * EL + e) * 64] = st.acc[h][e];
+                    for (int e = 0; e < EL; ++e) dst[(2 * GS + h * EL + e) * 64] = st.acc[h][e];
                 }
             }
             __syncthreads();
             if (wave < half) {
                 const float* src = merge_lds + (size_t)wave * NV * 64 + lane;
-                float bm[G], bl[G], bacc[G][EL];
+                float bm[GS], bl[GS], bacc[GS][EL];
 #pragma unroll
-                for (int h = 0; h < G; ++h) {
+                for (int h = 0; h < GS; ++h) {
                     bm[h] = src[(2 * h) * 64];
                     bl[h] = src[(2 * h + 1) * 64];
 #pragma unroll
-                    for (int e = 0; e < EL; ++e) bacc[h][e] = src[(2 * G + h * EL + e) * 64];
+                    for (int e = 0; e < EL; ++e) bacc[h][e] = src[(2 * GS + h * EL + e) * 64];
                 }
-                fold<BF16, D, G>(st, bm, bl, bacc);
+                fold<BF16, D, GS>(st, bm, bl, bacc);
             }
         }
         __syncthreads();                           // merge buffer reads done: chunks may restage
-        if (wave == 0) {
+        if (wave < NWG) {
             // merge the slots that hold the same KV head (different tokens of an iteration)
 #pragma unroll
-            for (int mask = 8 * HKV; mask < 64; mask <<= 1) {
-                float bm[G], bl[G], bacc[G][EL];
+            for (int mask = 8 * SV; mask < 64; mask <<= 1) {
+                float bm[GS], bl[GS], bacc[GS][EL];
 #pragma unroll
-                for (int h = 0; h < G; ++h) {
+                for (int h = 0; h < GS; ++h) {
                     bm[h] = __shfl_xor(st.m[h], mask);
                     bl[h] = __shfl_xor(st.l[h], mask);
 #pragma unroll
@@ -643,7 +688,7 @@ attention_kernel(AttnArgs a) {
                 // fold in a fixed order: the lower lane's state first
                 if (lane & mask) {
 #pragma unroll
-                    for (int h = 0; h < G; ++h) {
+                    for (int h = 0; h < GS; ++h) {
                         const float tm = st.m[h], tl = st.l[h];
                         st.m[h] = bm[h]; bm[h] = tm;
                         st.l[h] = bl[h]; bl[h] = tl;
@@ -655,13 +700,14 @@ attention_kernel(AttnArgs a) {
                         }
                     }
                 }
-                fold<BF16, D, G>(st, bm, bl, bacc);
+                fold<BF16, D, GS>(st, bm, bl, bacc);
             }
-            // partial of (workgroup w, sequence b): slot (token 0, KV head g) writes heads g*G..
+            // partial of (workgroup w, sequence b): slot (token 0, virtual head vh) writes
+            // query heads qh0 .. qh0 + GS - 1
             if (tk == 0) {
-                const size_t part = (size_t)(w + b) * a.Hq + (size_t)g * G;
+                const size_t part = (size_t)(w + b) * a.Hq + (size_t)qh0;
 #pragma unroll
-                for (int h = 0; h < G; ++h) {
+                for (int h = 0; h < GS; ++h) {
                     float* dst = a.part_acc + (part + h) * D;
 #pragma unroll
                     for (int c = 0; c < NC; ++c)
@@ -759,9 +805,10 @@ constexpr int state_floats() { return 2 * G + G * Row<BF16, D>::kPerLane; }
 
 template <bool BF16, int D, int G>
 size_t lds_bytes(const AttnArgs& a) {
-    const size_t chunk = (size_t)kChunk * (4 + 4 + 4 + 1);
-    const size_t merge = (size_t)(merge_one_round<BF16, D, G>() ? kWaves : kWaves / 2) *
-                         state_floats<BF16, D, G>() * 64 * 4;
+    const size_t chunk = (size_t)kChunk * (4 + 4 + 8 + 1);
+    constexpr int GS = G / split_of<G>();
+    const size_t merge = (size_t)(merge_one_round<BF16, D, GS>() ? kWaves : kWaves / 2) *
+                         state_floats<BF16, D, GS>() * 64 * 4;
     return (size_t)(((a.B + 1 + 3) & ~3) + kDurCache) * 4 + (chunk > merge ? chunk : merge);
 }
 

@@ -107,3 +107,17 @@ def test_token_scope_heavy_hitters_two_layers():
     s_cold, s_hot = gen.hh_relevance_bounds(w)
     assert s_cold < w.tau - H.MARGIN and s_hot / 2 > w.tau + H.MARGIN
     _parity(w, {})
+
+
+@pytest.mark.parametrize("relevance,scope", [("abs", "layer"), ("abs", "token"),
+                                             ("softmax", "layer"), ("softmax", "token")])
+def test_wide_query_groups(relevance, scope):
+    """64 query heads over 8 KV heads (G = 8): a lane keeps half of a KV head's
+    query heads, two waves share every token, and the two parts of each
+    token's score are summed after the tiles, for both readings of the score
+    and both state scopes."""
+    w0 = _multi(name="wide", n_layers=2, n_q_heads=64, n_kv_heads=8, head_dim=128, dtype="bf16",
+                prefill=[260, 130], steps=40, relevance=relevance, scope=scope)
+    softmax = relevance == "softmax"
+    w, att = _tuned(w0, 0.5 if softmax else 0.55, relative=softmax)
+    _parity(w, att)
