@@ -209,6 +209,17 @@ __device__ __forceinline__ void fold(SoftState<BF16, D, G>& a, const float* bm, 
 template <int G>
 constexpr int split_of() { return G >= 8 ? 2 : 1; }
 
+// Shapes the kernel handles: a token row (every KV head) goes into the cache
+// with one 16-byte piece per thread, and after the split no more waves share a
+// token than there are waves per state part to fold a head's rows.
+template <bool BF16, int D, int G, int HKV>
+constexpr bool shape_supported() {
+    constexpr int GS = G / split_of<G>();
+    constexpr int VH = HKV * split_of<G>();
+    constexpr int NWG = VH > 8 ? VH / 8 : 1;
+    return HKV * Row<BF16, D>::kBytes <= 64 * kWaves * 16 && NWG <= 4 && GS <= kWaves / NWG;
+}
+
 // All 8 wave states fit in LDS next to the other buffers: merge in one round.
 template <bool BF16, int D, int G>
 constexpr bool merge_one_round() {
@@ -238,7 +249,7 @@ attention_kernel(AttnArgs a) {
     constexpr int TT = kUnroll * TPI;            // tokens per tile
     constexpr int NV = 2 * GS + GS * EL;         // floats of a lane's state
     constexpr bool kOneRound = merge_one_round<BF16, D, GS>();
-    static_assert(HKV * R::kBytes <= 64 * kWaves * 16, "the appended row takes one piece per thread");
+    static_assert(shape_supported<BF16, D, G, HKV>(), "unsupported head layout");
 
     extern __shared__ int32_t lds[];
     __shared__ unsigned tile_lead;                               // most tiles any wave has finished
@@ -246,9 +257,9 @@ attention_kernel(AttnArgs a) {
     int32_t* dur_lds = lds + ((a.B + 1 + 3) & ~3);               // [kDurCache]
     int32_t* pos_lds = dur_lds + kDurCache;                      // [kChunk]
     int32_t* row_lds = pos_lds + kChunk;                         // [kChunk] (spill mode)
-    float* rel_lds = reinterpret_cast<float*>(row_lds + kChunk);   // [kChunk][NWG] (token scope;
-                                                                 // the parts' sums when NWG > 1)
-    uint8_t* flag_lds = reinterpret_cast<uint8_t*>(rel_lds + 2 * kChunk);   // [kChunk]
+    float* rel_lds = reinterpret_cast<float*>(row_lds + kChunk);   // [kChunk][NWG <= 4] (token
+                                                                 // scope; the parts' sums)
+    uint8_t* flag_lds = reinterpret_cast<uint8_t*>(rel_lds + 4 * kChunk);   // [kChunk]
     // the wave-state merge runs after the chunk loop: it reuses the chunk buffers
     float* merge_lds = reinterpret_cast<float*>(pos_lds);        // [kWaves/2][NV][64]
 
@@ -805,7 +816,7 @@ constexpr int state_floats() { return 2 * G + G * Row<BF16, D>::kPerLane; }
 
 template <bool BF16, int D, int G>
 size_t lds_bytes(const AttnArgs& a) {
-    const size_t chunk = (size_t)kChunk * (4 + 4 + 8 + 1);
+    const size_t chunk = (size_t)kChunk * (4 + 4 + 16 + 1);
     constexpr int GS = G / split_of<G>();
     const size_t merge = (size_t)(merge_one_round<BF16, D, GS>() ? kWaves : kWaves / 2) *
                          state_floats<BF16, D, GS>() * 64 * 4;
@@ -832,13 +843,21 @@ hipError_t launch_t(const AttnArgs& a, const Launch& l) {
                               args, lds, l.stream, l.start, l.stop, 0);
 }
 
+template <bool BF16, int D, int G, int HKV>
+hipError_t launch_s(const AttnArgs& a, const Launch& l) {
+    if constexpr (shape_supported<BF16, D, G, HKV>()) return launch_t<BF16, D, G, HKV>(a, l);
+    else return hipErrorInvalidValue;
+}
+
 template <bool BF16, int D, int G>
 hipError_t launch_h(const AttnArgs& a, const Launch& l) {
     switch (a.Hkv) {
-        case 1: return launch_t<BF16, D, G, 1>(a, l);
-        case 2: return launch_t<BF16, D, G, 2>(a, l);
-        case 4: return launch_t<BF16, D, G, 4>(a, l);
-        case 8: return launch_t<BF16, D, G, 8>(a, l);
+        case 1: return launch_s<BF16, D, G, 1>(a, l);
+        case 2: return launch_s<BF16, D, G, 2>(a, l);
+        case 4: return launch_s<BF16, D, G, 4>(a, l);
+        case 8: return launch_s<BF16, D, G, 8>(a, l);
+        case 16: return launch_s<BF16, D, G, 16>(a, l);
+        case 32: return launch_s<BF16, D, G, 32>(a, l);
     }
     return hipErrorInvalidValue;
 }
@@ -866,6 +885,39 @@ hipError_t dispatch(const AttnArgs& a, int dtype_bf16, int head_dim, int group, 
 }
 
 }  // namespace
+
+namespace {
+template <bool BF16, int D, int G>
+bool supported_h(int hkv) {
+    switch (hkv) {
+        case 1: return shape_supported<BF16, D, G, 1>();
+        case 2: return shape_supported<BF16, D, G, 2>();
+        case 4: return shape_supported<BF16, D, G, 4>();
+        case 8: return shape_supported<BF16, D, G, 8>();
+        case 16: return shape_supported<BF16, D, G, 16>();
+        case 32: return shape_supported<BF16, D, G, 32>();
+    }
+    return false;
+}
+template <bool BF16, int D>
+bool supported_g(int group, int hkv) {
+    switch (group) {
+        case 1: return supported_h<BF16, D, 1>(hkv);
+        case 2: return supported_h<BF16, D, 2>(hkv);
+        case 4: return supported_h<BF16, D, 4>(hkv);
+        case 8: return supported_h<BF16, D, 8>(hkv);
+    }
+    return false;
+}
+}  // namespace
+
+bool attention_shape_supported(int dtype_bf16, int head_dim, int group, int n_kv_heads) {
+    if (head_dim == 128) return dtype_bf16 ? supported_g<true, 128>(group, n_kv_heads)
+                                           : supported_g<false, 128>(group, n_kv_heads);
+    if (head_dim == 64) return dtype_bf16 ? supported_g<true, 64>(group, n_kv_heads)
+                                          : supported_g<false, 64>(group, n_kv_heads);
+    return false;
+}
 
 hipError_t launch_attention(const AttnArgs& a, int dtype_bf16, int head_dim, int group,
                             int grid, hipStream_t s, hipEvent_t start, hipEvent_t stop) {

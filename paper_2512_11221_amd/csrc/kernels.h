@@ -198,6 +198,8 @@ int compact_segments(int n_instances, int cap, int* seg_len);
 hipError_t launch_weight_relevance(const RelevanceArgs& a, hipStream_t s);
 hipError_t launch_spill_init(const SpillInitArgs& a, int n_instances, hipStream_t s);
 hipError_t launch_xfer(const XferArgs& a, int n_instances, hipStream_t s);
+// Whether the attention kernel handles this (dtype, head_dim, q heads per KV head, KV heads).
+bool attention_shape_supported(int dtype_bf16, int head_dim, int group, int n_kv_heads);
 hipError_t launch_delay(int microseconds, hipStream_t s);
 hipError_t launch_entropy(const EntropyArgs& a, hipStream_t s);
 

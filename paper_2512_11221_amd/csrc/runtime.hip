@@ -225,13 +225,20 @@ asrkf_status validate(const asrkf_config* c) {
     if (!c) return fail(ASRKF_EINVAL, "null config");
     if (c->n_layers < 1) return fail(ASRKF_EINVAL, "n_layers must be >= 1");
     if (c->batch < 1 || c->batch > kMaxBatch) return fail(ASRKF_EINVAL, "batch must be in 1..%d", kMaxBatch);
-    if (c->n_kv_heads != 1 && c->n_kv_heads != 2 && c->n_kv_heads != 4 && c->n_kv_heads != 8)
-        return fail(ASRKF_EINVAL, "n_kv_heads must be 1, 2, 4 or 8");
+    if (c->n_kv_heads != 1 && c->n_kv_heads != 2 && c->n_kv_heads != 4 && c->n_kv_heads != 8 &&
+        c->n_kv_heads != 16 && c->n_kv_heads != 32)
+        return fail(ASRKF_EINVAL, "n_kv_heads must be 1, 2, 4, 8, 16 or 32");
     if (c->n_q_heads < c->n_kv_heads || c->n_q_heads % c->n_kv_heads)
         return fail(ASRKF_EINVAL, "n_q_heads must be a multiple of n_kv_heads");
     const int g = c->n_q_heads / c->n_kv_heads;
     if (g != 1 && g != 2 && g != 4 && g != 8) return fail(ASRKF_EINVAL, "n_q_heads / n_kv_heads must be 1, 2, 4 or 8");
     if (c->head_dim != 64 && c->head_dim != 128) return fail(ASRKF_EINVAL, "head_dim must be 64 or 128");
+    if (c->dtype == ASRKF_BF16 || c->dtype == ASRKF_F32) {
+        if (!attention_shape_supported(c->dtype == ASRKF_BF16, c->head_dim, g, c->n_kv_heads))
+            return fail(ASRKF_EINVAL, "unsupported head layout: %d q heads over %d KV heads of %d %s",
+                        c->n_q_heads, c->n_kv_heads, c->head_dim,
+                        c->dtype == ASRKF_BF16 ? "bf16" : "fp32");
+    }
     if (c->max_ctx < 2 || c->max_ctx > (1 << 28)) return fail(ASRKF_EINVAL, "max_ctx must be in 2..2^28");
     if (c->window_K < 0) return fail(ASRKF_EINVAL, "window_K must be >= 0");
     if (isnan(c->tau)) return fail(ASRKF_EINVAL, "tau is NaN");

@@ -121,3 +121,14 @@ def test_wide_query_groups(relevance, scope):
     softmax = relevance == "softmax"
     w, att = _tuned(w0, 0.5 if softmax else 0.55, relative=softmax)
     _parity(w, att)
+
+
+@pytest.mark.parametrize("relevance,scope", [("abs", "layer"), ("softmax", "token")])
+def test_multi_head_attention(relevance, scope):
+    """32 query heads over 32 KV heads (plain multi-head attention): four waves
+    share every token, each with 8 of its KV heads."""
+    w0 = _multi(name="mha", n_layers=2, n_q_heads=32, n_kv_heads=32, head_dim=128, dtype="bf16",
+                prefill=[260, 130], steps=40, relevance=relevance, scope=scope)
+    softmax = relevance == "softmax"
+    w, att = _tuned(w0, 0.5 if softmax else 0.55, relative=softmax)
+    _parity(w, att)
