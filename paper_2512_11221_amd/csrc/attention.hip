@@ -28,6 +28,12 @@
 // reduced over the slot's 8 lanes with DPP, the relevance over the token's
 // KV-head slots with lane exchanges, so the freeze decision is made in the
 // wave and applied by the workgroup after each chunk.
+//
+// Wide groups and many KV heads.  With G = 8 a slot holds a virtual KV head,
+// one KV head with half of its query heads (two slots read the same row, in
+// the same load instruction).  When a token has more than 8 (virtual) heads,
+// 2 or 4 waves share each token, each with 8 of them; their parts of the
+// relevance sum meet in LDS after the tiles, where the flag is decided.
 #include "kernels.h"
 
 namespace asrkf {
