@@ -71,7 +71,7 @@ typedef struct {
     int32_t n_kv_heads;      /* 1, 2, 4, 8, 16 or 32; n_q_heads / n_kv_heads in {1, 2, 4, 8};
                                 with 16 KV heads at most 4 q heads per KV head, with 32 at
                                 most 2, and for fp32 rows of 128 at most 16 KV heads */
-    int32_t head_dim;        /* 64 or 128 */
+    int32_t head_dim;        /* 64, 128 or 256 (256 with bf16 rows only) */
     int32_t max_ctx;         /* positions per sequence: prompt + decode steps */
     int32_t window_K;        /* protected window of most recent positions (Sec. 3.2; paper: 32) */
     float   tau;             /* relevance threshold, strict s_j < tau (paper: 0.5) */

@@ -40,7 +40,6 @@ namespace asrkf {
 namespace {
 
 constexpr int kWaves = 8;           // waves per workgroup
-constexpr int kUnroll = 4;          // iterations per tile
 constexpr int kChunk = 2048;        // tokens per LDS chunk (positions, freeze flags)
 constexpr int kMinPerGroup = 32;    // fewest tokens worth a workgroup
 // Each sequence a workgroup takes part in costs it a fixed set-up and merge
@@ -91,6 +90,11 @@ struct Row {
     static constexpr int kPerChunk = 16 / kElem;
     static constexpr int kPerLane = kChunks * kPerChunk;  // = D / 8
 };
+
+// Iterations per tile: four, or two when a lane holds four pieces of a row
+// (bf16 rows of 256, fp32 rows of 128), so that a tile's rows stay in registers.
+template <bool BF16, int D>
+constexpr int tile_unroll() { return Row<BF16, D>::kChunks >= 4 ? 2 : 4; }
 
 template <bool BF16, int D>
 using Pieces = uint4[Row<BF16, D>::kChunks];      // the lane's 16-byte pieces of a row
@@ -210,20 +214,25 @@ __device__ __forceinline__ void fold(SoftState<BF16, D, G>& a, const float* bm, 
     }
 }
 
-// Query heads per KV head above which a lane keeps only half of them (the
-// softmax state of eight heads does not fit in a wave's registers).
-template <int G>
-constexpr int split_of() { return G >= 8 ? 2 : 1; }
+// How many parts a KV head's query heads are split into, so that a lane keeps
+// the softmax state of at most four heads (two for rows of 256): the state of
+// more does not fit in a wave's registers.
+template <bool BF16, int D, int G>
+constexpr int split_of() {
+    constexpr int kMaxHeads = Row<BF16, D>::kPerLane >= 32 ? 2 : 4;
+    return G > kMaxHeads ? G / kMaxHeads : 1;
+}
 
 // Shapes the kernel handles: a token row (every KV head) goes into the cache
 // with one 16-byte piece per thread, and after the split no more waves share a
 // token than there are waves per state part to fold a head's rows.
 template <bool BF16, int D, int G, int HKV>
 constexpr bool shape_supported() {
-    constexpr int GS = G / split_of<G>();
-    constexpr int VH = HKV * split_of<G>();
+    constexpr int GS = G / split_of<BF16, D, G>();
+    constexpr int VH = HKV * split_of<BF16, D, G>();
     constexpr int NWG = VH > 8 ? VH / 8 : 1;
-    return HKV * Row<BF16, D>::kBytes <= 64 * kWaves * 16 && NWG <= 4 && GS <= kWaves / NWG;
+    return (D != 256 || BF16) && HKV * Row<BF16, D>::kBytes <= 64 * kWaves * 16 && NWG <= 4 &&
+           GS <= kWaves / NWG;
 }
 
 // All 8 wave states fit in LDS next to the other buffers: merge in one round.
@@ -242,7 +251,8 @@ attention_kernel(AttnArgs a) {
     // virtual heads than a wave has slots, NWG waves share each token (wave
     // part p takes virtual heads 8p .. 8p + 7) and the relevance of the parts is
     // summed in LDS after the tiles.
-    constexpr int kSplit = split_of<G>();
+    constexpr int kSplit = split_of<BF16, D, G>();
+    constexpr int kUnroll = tile_unroll<BF16, D>();
     constexpr int GS = G / kSplit;               // query heads per lane
     constexpr int VH = HKV * kSplit;             // virtual KV heads
     constexpr int NWG = VH > 8 ? VH / 8 : 1;     // waves sharing a token
@@ -823,7 +833,7 @@ constexpr int state_floats() { return 2 * G + G * Row<BF16, D>::kPerLane; }
 template <bool BF16, int D, int G>
 size_t lds_bytes(const AttnArgs& a) {
     const size_t chunk = (size_t)kChunk * (4 + 4 + 16 + 1);
-    constexpr int GS = G / split_of<G>();
+    constexpr int GS = G / split_of<BF16, D, G>();
     const size_t merge = (size_t)(merge_one_round<BF16, D, GS>() ? kWaves : kWaves / 2) *
                          state_floats<BF16, D, GS>() * 64 * 4;
     return (size_t)(((a.B + 1 + 3) & ~3) + kDurCache) * 4 + (chunk > merge ? chunk : merge);
@@ -883,6 +893,7 @@ hipError_t dispatch(const AttnArgs& a, int dtype_bf16, int head_dim, int group, 
     if (dtype_bf16) {
         if (head_dim == 128) return launch_g<true, 128>(a, group, l);
         if (head_dim == 64) return launch_g<true, 64>(a, group, l);
+        if (head_dim == 256) return launch_g<true, 256>(a, group, l);
     } else {
         if (head_dim == 128) return launch_g<false, 128>(a, group, l);
         if (head_dim == 64) return launch_g<false, 64>(a, group, l);
@@ -922,6 +933,7 @@ bool attention_shape_supported(int dtype_bf16, int head_dim, int group, int n_kv
                                            : supported_g<false, 128>(group, n_kv_heads);
     if (head_dim == 64) return dtype_bf16 ? supported_g<true, 64>(group, n_kv_heads)
                                           : supported_g<false, 64>(group, n_kv_heads);
+    if (head_dim == 256) return dtype_bf16 && supported_g<true, 256>(group, n_kv_heads);
     return false;
 }
 

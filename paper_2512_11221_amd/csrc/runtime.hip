@@ -232,7 +232,8 @@ asrkf_status validate(const asrkf_config* c) {
         return fail(ASRKF_EINVAL, "n_q_heads must be a multiple of n_kv_heads");
     const int g = c->n_q_heads / c->n_kv_heads;
     if (g != 1 && g != 2 && g != 4 && g != 8) return fail(ASRKF_EINVAL, "n_q_heads / n_kv_heads must be 1, 2, 4 or 8");
-    if (c->head_dim != 64 && c->head_dim != 128) return fail(ASRKF_EINVAL, "head_dim must be 64 or 128");
+    if (c->head_dim != 64 && c->head_dim != 128 && c->head_dim != 256)
+        return fail(ASRKF_EINVAL, "head_dim must be 64, 128 or 256");
     if (c->dtype == ASRKF_BF16 || c->dtype == ASRKF_F32) {
         if (!attention_shape_supported(c->dtype == ASRKF_BF16, c->head_dim, g, c->n_kv_heads))
             return fail(ASRKF_EINVAL, "unsupported head layout: %d q heads over %d KV heads of %d %s",

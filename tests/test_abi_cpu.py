@@ -45,7 +45,7 @@ BASE = dict(n_layers=1, batch=1, n_q_heads=8, n_kv_heads=2, head_dim=64, max_ctx
 
 
 @pytest.mark.parametrize("bad", [
-    dict(head_dim=96), dict(n_kv_heads=3), dict(n_q_heads=24, n_kv_heads=2),
+    dict(head_dim=96), dict(head_dim=256, dtype="f32"), dict(n_kv_heads=3), dict(n_q_heads=24, n_kv_heads=2),
     dict(n_kv_heads=64, n_q_heads=64), dict(n_kv_heads=16, n_q_heads=128),
     dict(n_kv_heads=32, n_q_heads=128), dict(n_kv_heads=32, n_q_heads=32, head_dim=128, dtype="f32"),
     dict(batch=0), dict(batch=5000), dict(n_layers=0),

@@ -120,6 +120,9 @@ def test_bf16_gaussian_multilayer_ragged(tau):
     dict(n_q_heads=64, n_kv_heads=8, head_dim=128, dtype="bf16"),   # G = 8, two waves per token
     dict(n_q_heads=32, n_kv_heads=32, head_dim=128, dtype="bf16"),  # multi-head, four waves per token
     dict(n_q_heads=32, n_kv_heads=16, head_dim=64, dtype="bf16"),   # G = 2, two waves per token
+    dict(n_q_heads=16, n_kv_heads=16, head_dim=256, dtype="bf16"),  # rows of 256, multi-head
+    dict(n_q_heads=16, n_kv_heads=8, head_dim=256, dtype="bf16"),   # rows of 256, G = 2
+    dict(n_q_heads=32, n_kv_heads=8, head_dim=256, dtype="bf16"),   # rows of 256, G = 4 split
     dict(n_q_heads=8, n_kv_heads=4, head_dim=64, dtype="bf16"),     # G = 2, D = 64
     dict(n_q_heads=8, n_kv_heads=2, head_dim=128, dtype="f32"),     # fp32, D = 128
 ])
