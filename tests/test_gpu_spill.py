@@ -64,6 +64,18 @@ def test_flag_all_spills_and_restores():
     assert stats[-1]["rows_released"] > stats[-1]["rows_to_host"]   # rows re-released, not re-copied
 
 
+@pytest.mark.parametrize("shape", [
+    dict(n_q_heads=32, n_kv_heads=32, head_dim=128, dtype="bf16"),   # four waves share a token
+    dict(n_q_heads=64, n_kv_heads=8, head_dim=128, dtype="bf16"),    # G = 8 split in halves
+])
+def test_flag_all_spill_wide_layouts(shape):
+    """Spill mode with the head layouts in which several waves share each token:
+    released and restored rows are read through the device-row list."""
+    w = _flag_all(name="spill-wide", prefill=[300], steps=40, **shape)
+    g, o, _, stats = _spill_parity(w, H.Inputs(w))
+    assert stats[-1]["rows_from_host"] > 100
+
+
 def _resident_peak(w, inp):
     """Largest number of device rows the run needs: after each step, the
     positions not held only on the host, plus the next token (oracle states)."""
