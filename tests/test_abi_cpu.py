@@ -67,3 +67,23 @@ def test_null_context_is_einval():
     assert lib.asrkf_restore(None, None, 0, None) == A._lib.EINVAL
     assert "null context" in A.asrkf_last_error()
     lib.asrkf_destroy(None)
+
+
+def test_c_program_uses_the_abi(tmp_path):
+    """The header is plain C: a C99 program includes it, links libasrkf.so and
+    runs the host-only calls (tests/c_abi/abi_check.c)."""
+    import shutil
+    import subprocess
+    gcc = shutil.which("gcc")
+    if gcc is None:
+        pytest.skip("no C compiler")
+    lib = A.load()._name                       # the build the binding loads
+    exe = str(tmp_path / "abi_check")
+    subprocess.run([gcc, "-std=c99", "-Wall", "-Wextra", "-Werror", "-pedantic",
+                    os.path.join(ROOT, "tests", "c_abi", "abi_check.c"),
+                    "-I", os.path.join(ROOT, "include"), lib,
+                    "-Wl,-rpath-link,/opt/rocm/lib", "-o", exe],
+                   check=True, capture_output=True, text=True)
+    r = subprocess.run([exe], capture_output=True, text=True, timeout=60)
+    assert r.returncode == 0, r.stderr
+    assert "C ABI checks passed" in r.stdout
