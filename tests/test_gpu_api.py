@@ -115,3 +115,16 @@ def test_sequence_without_prompt_and_stats():
     assert abs(last["compression"] - (1 - n_active / n_total)) < 1e-12
     attended = sum(len(r["attended"]) for key in inst for r in o[key])
     assert last["attended_total"] == attended
+
+
+def test_c_program_drives_the_gpu():
+    """tests/c_abi/abi_gpu_check.c: a C program with HIP device buffers and no
+    Python runs 12 dense steps through the ABI and checks every output against
+    its own double-precision attention, plus the statistics."""
+    import os
+    import subprocess
+    exe = os.path.join(os.path.dirname(os.path.abspath(__file__)), "c_abi", "abi_gpu_check")
+    assert os.path.exists(exe), "build it first: __graft_entry__.build()"
+    r = subprocess.run([exe], capture_output=True, text=True, timeout=120)
+    assert r.returncode == 0, r.stdout + r.stderr
+    assert "C ABI GPU run passed" in r.stdout
