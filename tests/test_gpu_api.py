@@ -128,3 +128,63 @@ def test_c_program_drives_the_gpu():
     r = subprocess.run([exe], capture_output=True, text=True, timeout=120)
     assert r.returncode == 0, r.stdout + r.stderr
     assert "C ABI GPU run passed" in r.stdout
+
+
+def _tiny_freezing(seed_shift=0, **kw):
+    w0 = gen.tiny(seed=gen.SEED + 1 + seed_shift)
+    w = gen.tiny(seed=gen.SEED + 1 + seed_shift, tau=H.score_quantile(w0, 0.6), **kw)
+    return w, H.Inputs(w, H.fix_margin(w))
+
+
+def test_non_default_stream_gives_the_same_results():
+    """Every call queued on a stream of the caller's (torch's current stream
+    inside the context manager) gives bitwise the results of the default
+    stream."""
+    import torch
+    w, inp = _tiny_freezing()
+    a, _, _ = H.run_gpu(w, inp, [(0, 0)])
+    s = torch.cuda.Stream()
+    with torch.cuda.stream(s):
+        b, _, _ = H.run_gpu(w, inp, [(0, 0)])
+    torch.cuda.synchronize()
+    for x, y in zip(a[(0, 0)], b[(0, 0)]):
+        np.testing.assert_array_equal(x["out"], y["out"])
+        np.testing.assert_array_equal(x["active"], y["active"])
+
+
+def test_two_contexts_interleaved():
+    """Two contexts with different inputs, stepped alternately, each give
+    bitwise the outputs of a run alone: the library keeps no state outside a
+    context."""
+    import torch
+    import paper_2512_11221_amd as A
+    runs = [_tiny_freezing(0), _tiny_freezing(7)]
+    alone = [H.run_gpu(w, inp, [(0, 0)])[0][(0, 0)] for w, inp in runs]
+    ctxs = []
+    try:
+        for w, inp in runs:
+            cfg = A.make_config(w.n_layers, w.batch, w.n_q_heads, w.n_kv_heads, w.head_dim,
+                                w.max_ctx, w.window_K, w.tau, w.k_soft, w.vocab,
+                                entropy_spike=w.entropy_spike, conf_drop=w.conf_drop,
+                                wr_last_N=w.wr_last_N, dtype=w.dtype)
+            ctx = A.asrkf_init(cfg)
+            ctxs.append(ctx)
+            K, V = inp.prompt(0, 0)
+            A.asrkf_prefill(ctx, 0, 0, H._dev(K, w.dtype), H._dev(V, w.dtype), len(K))
+        torch.cuda.synchronize()
+        outs = [[], []]
+        for t in range(1, runs[0][0].steps + 1):
+            for i, (w, inp) in enumerate(runs):
+                q = H._dev(inp.q(0, 0, t)[None], w.dtype)
+                kn, vn = inp.new_token(0, 0, t)
+                out = torch.empty((1, w.n_q_heads, w.head_dim), dtype=torch.float32, device="cuda")
+                A.asrkf_decode_step(ctxs[i], 0, q, H._dev(kn[None], w.dtype), H._dev(vn[None], w.dtype), out)
+                A.asrkf_restore(ctxs[i], H._dev(inp.logits(0, t)[None], "f32"), A.AUTO)
+                torch.cuda.synchronize()
+                outs[i].append(out.cpu().numpy()[0])
+        for i in range(2):
+            for rec, o in zip(alone[i], outs[i]):
+                np.testing.assert_array_equal(rec["out"], o)
+    finally:
+        for ctx in ctxs:
+            A.asrkf_destroy(ctx)
