@@ -166,3 +166,31 @@ def test_bitwise_determinism():
         np.testing.assert_array_equal(x["out"], y["out"])
         np.testing.assert_array_equal(x["unfreeze"], y["unfreeze"])
         np.testing.assert_array_equal(x["active"], y["active"])
+
+
+_LAYOUTS = [  # (q heads, KV heads, head_dim, dtype), every layout family the kernel has
+    (8, 2, 64, "f32"), (8, 8, 128, "bf16"), (32, 8, 128, "bf16"), (16, 2, 128, "bf16"),
+    (64, 8, 128, "bf16"), (32, 32, 128, "bf16"), (32, 16, 64, "bf16"), (16, 8, 256, "bf16"),
+    (4, 4, 64, "f32"), (2, 1, 128, "bf16"), (64, 32, 64, "bf16"), (16, 16, 256, "bf16"),
+]
+
+
+@pytest.mark.parametrize("case", range(len(_LAYOUTS)))
+def test_seeded_random_runs(case):
+    """For each head layout, a run whose sizes are drawn from a seeded generator:
+    2-4 sequences with prompts of 0..700 tokens, 1-2 layers, a window of 0..40
+    and k in [0.5, 3], every out-of-window token flagged each step (tau = +inf)
+    or none (tau = -inf), so that freezing, restores and the planner's ranges
+    all vary while no score sits near tau."""
+    rng = np.random.default_rng([0x2512, case])
+    hq, hkv, d, dtype = _LAYOUTS[case]
+    batch = int(rng.integers(2, 5))
+    w = gen.Workload(name=f"random-{case}", seed=gen.SEED + 200 + case,
+                     n_layers=int(rng.integers(1, 3)), batch=batch, n_q_heads=hq, n_kv_heads=hkv,
+                     head_dim=d, dtype=dtype,
+                     prefill=[int(x) for x in rng.integers(0, 700, size=batch)],
+                     steps=int(rng.integers(12, 30)), window_K=int(rng.integers(0, 41)),
+                     tau=math.inf if case % 3 else -math.inf,
+                     k_soft=float(np.round(rng.uniform(0.5, 3.0), 2)), vocab=64, logit_sigma=1.0,
+                     recipe="gauss")
+    _parity(w, H.Inputs(w))
