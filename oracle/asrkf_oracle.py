@@ -35,7 +35,8 @@ design notes with the evidence for it):
   attention weight (mean over heads of the softmax weights) instead of Eq. 2's
   |q . k|; token-global scope (one token state per sequence shared by all
   layers, relevance averaged over layers) instead of per-(layer, sequence)
-  states;
+  states; freeze candidates taken inside the window of the K most recent
+  positions (the wording of Sec. 3.2) instead of outside it;
 * recovery (parity unpinned: the paper proposes but never evaluates it):
   a step whose entropy exceeds theta_H (or whose top probability falls below
   theta_p when theta_p > 0) raises the sequence's escalation count by one, a
@@ -195,10 +196,18 @@ class TokenStates:
 
     history_W = 0 counts every detection (c_j cumulative); history_W = W > 0
     counts the detections of the last W steps only (Eq. 3's history window):
-    at a detection in step t, c_j = number of detections in steps t-W+1 .. t."""
+    at a detection in step t, c_j = number of detections in steps t-W+1 .. t.
 
-    def __init__(self, cap, window_K, tau, k_soft, history_W=0):
+    candidates "outside" takes the freeze candidates among the active tokens
+    outside the window of the K most recent positions (Algorithm 1's freeze
+    loop); "inside" takes them among the active tokens inside that window (the
+    wording of Sec. 3.2, which estimates relevance within the window)."""
+
+    def __init__(self, cap, window_K, tau, k_soft, history_W=0, candidates="outside"):
+        if candidates not in ("outside", "inside"):
+            raise ValueError(f"candidates must be 'outside' or 'inside', not {candidates!r}")
         self.n = 0
+        self.candidates = candidates
         self.t = 0                                      # current step
         self.window_K = int(window_K)
         self.tau = float(tau)
@@ -228,6 +237,10 @@ class TokenStates:
         (the window includes the token appended this step)."""
         return j < self.n - self.window_K
 
+    def is_candidate(self, j):
+        """True when position j may be frozen by the freeze loop."""
+        return self.outside_window(j) if self.candidates == "outside" else not self.outside_window(j)
+
     def detect(self, j):
         """Record a low-relevance detection of j at the current step; returns c_j."""
         if not self.history_W:
@@ -239,10 +252,11 @@ class TokenStates:
         return self.count[j]
 
     def freeze_loop(self, A, s):
-        """For j outside the sliding window with s_j < tau: c_j += 1,
-        d_j = floor(sqrt(c_j)/k), and if d_j > 0 move j from A to F."""
+        """For each candidate j (by default: outside the sliding window) with
+        s_j < tau: c_j += 1, d_j = floor(sqrt(c_j)/k), and if d_j > 0 move j
+        from A to F."""
         for j, sj in zip(A, s):
-            if self.outside_window(j) and sj < self.tau:
+            if self.is_candidate(j) and sj < self.tau:
                 self.timer[j] = self._duration(self.detect(j))
                 if self.timer[j] > 0:
                     self.frozen[j] = True
@@ -310,10 +324,10 @@ class Instance(TokenStates):
     relevance_kind "abs" is Eq. 2; "softmax" scores by attention weights."""
 
     def __init__(self, K_prompt, V_prompt, window_K, tau, k_soft, capacity=None,
-                 history_W=0, relevance_kind="abs"):
+                 history_W=0, relevance_kind="abs", candidates="outside"):
         P = len(K_prompt)
         cap = capacity if capacity is not None else P + 4096
-        super().__init__(cap, window_K, tau, k_soft, history_W)
+        super().__init__(cap, window_K, tau, k_soft, history_W, candidates)
         self.cache = LayerCache(K_prompt, V_prompt, cap, relevance_kind)
         self.K, self.V = self.cache.K, self.cache.V
         self.n = P
@@ -339,10 +353,10 @@ class GlobalInstance(TokenStates):
     over that layer's heads), i.e. the mean over layers x heads."""
 
     def __init__(self, K_prompts, V_prompts, window_K, tau, k_soft, capacity=None,
-                 history_W=0, relevance_kind="abs"):
+                 history_W=0, relevance_kind="abs", candidates="outside"):
         P = len(K_prompts[0])
         cap = capacity if capacity is not None else P + 4096
-        super().__init__(cap, window_K, tau, k_soft, history_W)
+        super().__init__(cap, window_K, tau, k_soft, history_W, candidates)
         self.caches = [LayerCache(K, V, cap, relevance_kind) for K, V in zip(K_prompts, V_prompts)]
         self.n = P
 

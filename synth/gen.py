@@ -122,7 +122,8 @@ class Workload:
                  dtype, prefill, steps, window_K, tau, k_soft, vocab, logit_sigma,
                  recipe, f_hh=0.0, entropy_spike=float("inf"), conf_drop=0.0,
                  wr_last_N=None, flat_logit_steps=(), flat_sigma=0.1, spill_min_D=0,
-                 max_ctx=None, device_rows=0, history_W=0, relevance="abs", scope="layer"):
+                 max_ctx=None, device_rows=0, history_W=0, relevance="abs", scope="layer",
+                 candidates="outside"):
         self.name = name
         self.seed = int(seed)
         self.n_layers = int(n_layers)
@@ -151,6 +152,7 @@ class Workload:
         self.history_W = int(history_W)
         self.relevance = relevance              # "abs" (Eq. 2) or "softmax" (attention weight)
         self.scope = scope                      # "layer" or "token"
+        self.candidates = candidates            # freeze candidates "outside" or "inside" the window
         self.max_ctx = int(max_ctx if max_ctx is not None else max(self.prefill) + self.steps)
 
     @property

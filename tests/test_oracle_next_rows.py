@@ -210,3 +210,98 @@ def test_planted_unscaled_softmax_breaks_logistic(monkeypatch):
     monkeypatch.setattr(O, "relevance_softmax", unscaled)
     with pytest.raises(AssertionError):
         test_softmax_relevance_two_tokens_is_logistic()
+
+
+# --------------------------------------------------------------------------
+# freeze candidates inside the window (the wording of Sec. 3.2)
+# --------------------------------------------------------------------------
+
+def _flag_all_inside(P, steps, K, k_soft, cls=O.Instance, hook=None):
+    inst = cls(np.zeros((P, 1, 1)), np.zeros((P, 1, 1)), K, math.inf, k_soft,
+               capacity=P + steps + 1, candidates="inside")
+    z = np.zeros((1, 1))
+    for t in range(1, steps + 1):
+        rec = inst.step(z, z, z)
+        if hook:
+            hook(t, rec, inst)
+    return inst
+
+
+@pytest.mark.parametrize("P", [0, 1, 14, 40, 100])
+def test_inside_window_frozen_at_end(P):
+    g = _golden("inside_window_trajectory.json")
+    for K, frozen in g["frozen_at_end_by_K"]:
+        for steps in (K + 2, K + 37, 150):
+            inst = _flag_all_inside(P, steps, K, g["k"])
+            assert int(inst.frozen[: inst.n].sum()) == frozen, (P, K, steps)
+
+
+def test_inside_window_token_trajectory():
+    g = _golden("inside_window_trajectory.json")
+    tr = g["token_appended_at_step_1"]
+    P = 14
+    attends = set()
+    _flag_all_inside(P, 220, tr["K"], g["k"],
+                     hook=lambda t, rec, inst: attends.add(t) if P in rec.active else None)
+    for t in tr["excluded_at_steps"]:
+        assert t not in attends, t
+    for t in tr["attends_at_steps"]:
+        assert t in attends, t
+    excluded = set(range(1, 221)) - attends
+    assert excluded == set(tr["excluded_at_steps"])
+
+
+def test_inside_window_table_runs():
+    g = _golden("inside_window_trajectory.json")
+    for n, active in g["table_runs"]:
+        inst = _flag_all_inside(14, n - 14, 32, g["k"])
+        assert inst.n == n and int((~inst.frozen[:n]).sum()) == active
+
+
+def test_inside_window_only_window_tokens_are_counted():
+    """Tokens outside the window are never detected: their counts stop when
+    they leave it, and the protected region of the default reading is exactly
+    where detections happen now."""
+    inst = _flag_all_inside(20, 120, 8, 2.0)
+    n = inst.n
+    assert (inst.count[: n - 8] <= 8).all()
+    assert (inst.count[20: n - 8] == 8).all()        # decode tokens: 8 steps inside, never frozen
+
+
+def test_inside_window_token_scope_matches_layer_scope_when_all_flagged():
+    P, steps, K = 14, 90, 32
+    a = _flag_all_inside(P, steps, K, 2.0)
+    L = 3
+    z = np.zeros((P, 1, 1))
+    gi = O.GlobalInstance([z] * L, [z] * L, K, math.inf, 2.0, capacity=P + steps + 1,
+                          candidates="inside")
+    q = np.zeros((1, 1))
+    for _ in range(steps):
+        gi.step([q] * L, [q] * L, [q] * L)
+    assert (gi.frozen[: gi.n] == a.frozen[: a.n]).all()
+    assert (gi.count[: gi.n] == a.count[: a.n]).all()
+
+
+def test_unknown_candidates_value_is_refused():
+    with pytest.raises(ValueError):
+        O.Instance(np.zeros((1, 1, 1)), np.zeros((1, 1, 1)), 4, 0.0, 2.0, candidates="all")
+
+
+class _InsideWindowOneWider(O.Instance):
+    """Planted: a window of K + 1 positions."""
+    def outside_window(self, j):
+        return j < self.n - 1 - self.window_K
+
+
+class _InsideWindowOneNarrower(O.Instance):
+    """Planted: the window leaves out the token appended this step."""
+    def outside_window(self, j):
+        return j < self.n - self.window_K or j == self.n - 1
+
+
+@pytest.mark.parametrize("cls", [_InsideWindowOneWider, _InsideWindowOneNarrower])
+def test_planted_inside_window_edges_break_the_hand_counts(cls):
+    g = _golden("inside_window_trajectory.json")
+    got = [int(_flag_all_inside(14, 120, K, g["k"], cls=cls).frozen.sum())
+           for K, _ in g["frozen_at_end_by_K"]]
+    assert got != [f for _, f in g["frozen_at_end_by_K"]]
