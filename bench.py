@@ -39,6 +39,8 @@ def parse():
     ap.add_argument("--scope", choices=["layer", "token"], default=None,
                     help="token-state scope (default: per layer and sequence)")
     ap.add_argument("--history-W", type=int, default=None, help="detection-count window (0 = all)")
+    ap.add_argument("--candidates", choices=["outside", "inside"], default=None,
+                    help="freeze candidates relative to the K-recent window (default: outside)")
     ap.add_argument("--layers", type=int, default=0,
                     help="run only the first N layers of the workload (counter runs); 0 = all")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",
@@ -83,7 +85,9 @@ def cpu_baseline(w, budget_s):
         threads = 1
     P = w.prefill[0]
     K, V = gen.kv_rows(w, 0, 0, 0, P + w.steps)
-    inst = oracle.Instance(K[:P], V[:P], w.window_K, w.tau, w.k_soft, capacity=P + w.steps + 1)
+    inst = oracle.Instance(K[:P], V[:P], w.window_K, w.tau, w.k_soft, capacity=P + w.steps + 1,
+                           history_W=w.history_W, relevance_kind=w.relevance,
+                           candidates=w.candidates)
     attended, spent, steps = 0, 0.0, 0
     for t in range(1, w.steps + 1):
         q = gen.q_row(w, 0, 0, t)
@@ -124,7 +128,7 @@ def main():
     w = getattr(gen, WORKLOADS[args.workload])(steps=W + K)
     if args.layers:
         w = w.replace(n_layers=min(args.layers, w.n_layers))
-    for key in ("relevance", "scope", "history_W"):
+    for key in ("relevance", "scope", "history_W", "candidates"):
         if getattr(args, key) is not None:
             w = w.replace(**{key: getattr(args, key)})
     L, B, Hq, Hkv, D = w.n_layers, w.batch, w.n_q_heads, w.n_kv_heads, w.head_dim
@@ -133,7 +137,8 @@ def main():
     cfg = A.make_config(L, B, Hq, Hkv, D, w.max_ctx, w.window_K, w.tau, w.k_soft, w.vocab,
                         entropy_spike=w.entropy_spike, conf_drop=w.conf_drop,
                         wr_last_N=w.wr_last_N, dtype=w.dtype, spill_min_D=w.spill_min_D,
-                        history_W=w.history_W, relevance=w.relevance, scope=w.scope)
+                        history_W=w.history_W, relevance=w.relevance, scope=w.scope,
+                        candidates=w.candidates)
     dg = DeviceGen(w)
     S = W + K
     Q = torch.empty((S, L, B, Hq, D), dtype=tdt, device="cuda")
@@ -209,7 +214,7 @@ def main():
     attn_s = st_timed["attn_kernel_ms"] / 1e3
     achieved = bytes_per_token * attended / attn_s / 1e9
     default_path = (w.relevance == "abs" and w.scope == "layer" and not w.history_W
-                    and not w.spill_min_D)
+                    and not w.spill_min_D and w.candidates == "outside")
     traffic = measured_traffic(w.name, K, W) if default_path else None
     traffic, traffic_layers = traffic if traffic else (None, None)
     if args.copy_calibration > 0:
@@ -236,7 +241,8 @@ def main():
                    if len(set(w.prefill)) == 1 else "ragged", "q_heads": Hq, "kv_heads": Hkv,
                    "head_dim": D, "window_K": w.window_K, "tau": w.tau, "k": w.k_soft,
                    "vocab": w.vocab, "mode": "spill" if w.spill_min_D else "resident",
-                   "relevance": w.relevance, "scope": w.scope, "history_W": w.history_W},
+                   "relevance": w.relevance, "scope": w.scope, "history_W": w.history_W,
+                   "candidates": w.candidates},
         "decode_steps_per_s": K / elapsed,
         "hbm_fraction_step": algo_bytes / elapsed / 1e9 / PEAK_HBM_GBS,
         "attended_fraction": attended / max(1, sum(p + t for p in w.prefill

@@ -64,6 +64,12 @@ typedef enum { ASRKF_REL_ABS = 0, ASRKF_REL_SOFTMAX = 1 } asrkf_relevance;
 /* Scope of the token states. */
 typedef enum { ASRKF_SCOPE_LAYER = 0, ASRKF_SCOPE_TOKEN = 1 } asrkf_scope;
 
+/* Where the freeze loop takes its candidates, relative to the window of the
+ * window_K most recent positions (the window includes the token appended this
+ * step).  Algorithm 1 freezes tokens outside the window; Sec. 3.2 words the
+ * estimate as made within the window. */
+typedef enum { ASRKF_CAND_OUTSIDE = 0, ASRKF_CAND_INSIDE = 1 } asrkf_candidates;
+
 typedef struct {
     int32_t n_layers;        /* >= 1 */
     int32_t batch;           /* sequences, 1 .. 1024 */
@@ -104,6 +110,9 @@ typedef struct {
                                 ASRKF_SCOPE_TOKEN: one token state per sequence shared by
                                 every layer (a frozen token leaves all layers), scored by
                                 the mean of its per-layer relevance.  Not with spill mode. */
+    int32_t candidates;      /* ASRKF_CAND_OUTSIDE (0, Algorithm 1): active tokens at positions
+                                < n_t - window_K may freeze; ASRKF_CAND_INSIDE: active tokens at
+                                positions >= n_t - window_K may freeze instead */
 } asrkf_config;
 
 typedef struct {

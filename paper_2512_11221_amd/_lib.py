@@ -19,6 +19,7 @@ BF16, F32 = 0, 1
 AUTO, SR, WR, FR, NONE = 0, 1, 2, 3, 4
 REL_ABS, REL_SOFTMAX = 0, 1
 SCOPE_LAYER, SCOPE_TOKEN = 0, 1
+CAND_OUTSIDE, CAND_INSIDE = 0, 1
 _STATUS = {EINVAL: "EINVAL", ENOMEM: "ENOMEM", EHIP: "EHIP", ESTATE: "ESTATE",
            ECAPACITY: "ECAPACITY"}
 
@@ -34,6 +35,7 @@ class asrkf_config(ctypes.Structure):
         ("dtype", ctypes.c_int32), ("spill_min_D", ctypes.c_int32),
         ("device_rows", ctypes.c_int32), ("history_W", ctypes.c_int32),
         ("relevance", ctypes.c_int32), ("scope", ctypes.c_int32),
+        ("candidates", ctypes.c_int32),
     ]
 
 
@@ -121,15 +123,28 @@ def _stream(s):
     return s.cuda_stream
 
 
+def _enum(name, value, names):
+    """A string option by name, or an int passed through unchanged (the
+    library checks it)."""
+    if isinstance(value, int):
+        return value
+    if value not in names:
+        raise ValueError(f"{name} must be one of {sorted(names)}, not {value!r}")
+    return names[value]
+
+
 def make_config(n_layers, batch, n_q_heads, n_kv_heads, head_dim, max_ctx, window_K, tau,
                 k_soft, vocab, entropy_spike=math.inf, conf_drop=0.0, wr_last_N=0,
                 dtype="bf16", spill_min_D=0, device_rows=0, history_W=0, relevance="abs",
-                scope="layer"):
+                scope="layer", candidates="outside"):
     return asrkf_config(n_layers, batch, n_q_heads, n_kv_heads, head_dim, max_ctx, window_K,
                         tau, k_soft, vocab, entropy_spike, conf_drop, wr_last_N,
-                        BF16 if dtype == "bf16" else F32, spill_min_D, device_rows, history_W,
-                        REL_SOFTMAX if relevance == "softmax" else REL_ABS,
-                        SCOPE_TOKEN if scope == "token" else SCOPE_LAYER)
+                        _enum("dtype", dtype, {"bf16": BF16, "f32": F32}),
+                        spill_min_D, device_rows, history_W,
+                        _enum("relevance", relevance, {"abs": REL_ABS, "softmax": REL_SOFTMAX}),
+                        _enum("scope", scope, {"layer": SCOPE_LAYER, "token": SCOPE_TOKEN}),
+                        _enum("candidates", candidates,
+                              {"outside": CAND_OUTSIDE, "inside": CAND_INSIDE}))
 
 
 def asrkf_init(cfg):

@@ -369,6 +369,7 @@ attention_kernel(AttnArgs a) {
             }
             const int n_pos = a.plen[b] + a.t;       // positions after the append
             const int wedge = n_pos - a.window_K;    // positions < wedge are outside the window
+            const bool inside = a.cand_inside != 0;
             // stage the chunk's positions (and device rows): every load first, then the
             // stores; the query rows are requested in between, so the chunk's set-up
             // costs one memory round trip
@@ -468,7 +469,7 @@ attention_kernel(AttnArgs a) {
                                 rel_lds[(tb + u * TPI + tk) * NWG + wpart] = rel;
                             } else if (scope_token) {
                                 rel_lds[tb + u * TPI + tk] = rel;
-                            } else if (pos[u] < wedge && rel < a.tau_H) {
+                            } else if (rel < a.tau_H) {   // candidates are sorted out below
                                 flag_lds[tb + u * TPI + tk] = 1;
                             }
                         }
@@ -540,7 +541,7 @@ attention_kernel(AttnArgs a) {
 #pragma unroll
                         for (int p2 = 0; p2 < NWG; ++p2) sum += rel_lds[i * NWG + p2];
                         if (scope_token) rel_lds[i * NWG] = sum;
-                        else flag_lds[i] = rel_abs && pos_lds[i] < wedge && sum < a.tau_H;
+                        else flag_lds[i] = rel_abs && sum < a.tau_H;
                     }
                 }
             }
@@ -558,7 +559,9 @@ attention_kernel(AttnArgs a) {
                     if (i < len) a.rel_acc[seq_row + pos_lds[i]] = prev[k] + rel_lds[i * NWG];
                 }
             }
-            // freeze loop over the chunk's flagged tokens (Alg. 1; Eq. 3)
+            // freeze loop over the chunk's flagged candidates (Alg. 1; Eq. 3); a flag
+            // says only that the score is below tau, the window test is made here,
+            // outside the tile loop
             if (a.history_W == 0) {
                 // cumulative count: every count load first, then the updates
                 // (an entry without a flag reads the sequence's first count and ignores it)
@@ -567,8 +570,9 @@ attention_kernel(AttnArgs a) {
 #pragma unroll
                 for (int k = 0; k < kStage; ++k) {
                     const int i = threadIdx.x + k * 64 * kWaves;
-                    f[k] = i < len && flag_lds[i];
-                    p[k] = f[k] ? pos_lds[i] : 0;
+                    const int pi = pos_lds[min(i, len - 1)];
+                    f[k] = i < len && flag_lds[i] && freeze_candidate(pi, wedge, inside);
+                    p[k] = f[k] ? pi : 0;
                 }
 #pragma unroll
                 for (int k = 0; k < kStage; ++k) cnt[k] = a.count[seq_row + p[k]];
@@ -583,7 +587,7 @@ attention_kernel(AttnArgs a) {
                 }
             } else {
                 for (int i = threadIdx.x; i < len; i += blockDim.x) {
-                    if (!flag_lds[i]) continue;
+                    if (!flag_lds[i] || !freeze_candidate(pos_lds[i], wedge, inside)) continue;
                     const size_t o = seq_row + pos_lds[i];
                     const int c = detect(a.count, a.hmask, a.hlast, o, a.t, a.history_W);
                     const int d = c < kDurCache ? dur_lds[c] : a.dur[min(c, a.dur_len - 1)];

@@ -138,7 +138,8 @@ __device__ int compact_range(const CompactArgs& a, const Ladder& r, size_t base,
 #pragma unroll
                 for (int k = 0; k < 4; ++k) {
                     const int q = p + k;
-                    if (q < hi && u[k] <= a.t && q < n - a.window_K && a.rel_acc[base + q] < a.tau_LH) {
+                    if (q < hi && u[k] <= a.t && freeze_candidate(q, n - a.window_K, a.cand_inside != 0) &&
+                        a.rel_acc[base + q] < a.tau_LH) {
                         const int c = detect(a.count, a.hmask, a.hlast, base + q, a.t, a.history_W);
                         const int d = a.dur[min(c, a.dur_len - 1)];
                         if (d >= 1) {

@@ -35,6 +35,14 @@ __device__ __forceinline__ int detect(int32_t* count, uint64_t* hmask, int32_t* 
     return c;
 }
 
+// Whether the token at position pos may be frozen.  wedge = n_t - K: positions
+// >= wedge form the window of the K most recent positions (Sec. 3.2), which
+// includes the token appended this step.  Algorithm 1 takes the candidates
+// outside the window; inside = true takes those inside it instead.
+__device__ __forceinline__ bool freeze_candidate(int pos, int wedge, bool inside) {
+    return (pos < wedge) != inside;
+}
+
 struct AttnArgs {
     const void* kpool;        // layer base, [B][pool_rows][Hkv][D]
     const void* vpool;
@@ -60,6 +68,7 @@ struct AttnArgs {
     int32_t spill;            // 1: rows come from list_row
     int32_t t;                // current step (1-based)
     int32_t window_K;
+    int32_t cand_inside;      // 1: freeze candidates inside the window, 0: outside
     int32_t dur_len;
     float tau_H;              // tau * Hq: compared against sum_h |q_h . k_j|
     float scale_log2;         // log2(e) / sqrt(D)
@@ -101,6 +110,7 @@ struct RelevanceArgs {
     const int32_t* dur;
     float* rel_acc;           // token scope [B][cap]
     int32_t B, cap, Hq, t, window_K, dur_len, history_W, scope_token, first_layer;
+    int32_t cand_inside;      // 1: freeze candidates inside the window, 0: outside
     float tau_H;
 };
 
@@ -139,6 +149,7 @@ struct CompactArgs {
     int32_t* hlast;
     const int32_t* dur;
     int32_t dur_len, history_W, window_K;
+    int32_t cand_inside;      // 1: freeze candidates inside the window, 0: outside
     // segmented rebuild of few, long instances (n_seg > 1)
     int32_t n_seg, seg_len;
     int32_t* seg_count;       // [instances][n_seg] counts ([instances][n_seg + 1][4] in spill mode)

@@ -36,7 +36,7 @@ weight_relevance_kernel(RelevanceArgs a) {
         const size_t o = row + pos;
         if (a.scope_token) {
             a.rel_acc[o] = a.first_layer ? s : a.rel_acc[o] + s;
-        } else if (pos < wedge && s < a.tau_H) {
+        } else if (freeze_candidate(pos, wedge, a.cand_inside != 0) && s < a.tau_H) {
             const int c = detect(a.count, a.hmask, a.hlast, o, a.t, a.history_W);
             const int d = a.dur[min(c, a.dur_len - 1)];
             if (d >= 1) a.unfreeze[o] = a.t + d;

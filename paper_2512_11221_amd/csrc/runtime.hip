@@ -253,6 +253,8 @@ asrkf_status validate(const asrkf_config* c) {
         return fail(ASRKF_EINVAL, "unknown relevance kind");
     if (c->scope != ASRKF_SCOPE_LAYER && c->scope != ASRKF_SCOPE_TOKEN)
         return fail(ASRKF_EINVAL, "unknown state scope");
+    if (c->candidates != ASRKF_CAND_OUTSIDE && c->candidates != ASRKF_CAND_INSIDE)
+        return fail(ASRKF_EINVAL, "unknown freeze candidates");
     if (c->scope == ASRKF_SCOPE_TOKEN && c->spill_min_D != 0)
         return fail(ASRKF_EINVAL, "spill mode needs per-layer token states (ASRKF_SCOPE_LAYER)");
     if (c->spill_min_D == 0 && c->device_rows != 0)
@@ -510,6 +512,7 @@ asrkf_status build_lists(asrkf_ctx* ctx, int forced_level, hipStream_t s) {
         a.dur_len = ctx->dur_len;
         a.history_W = ctx->cfg.history_W;
         a.window_K = ctx->cfg.window_K;
+        a.cand_inside = ctx->cfg.candidates == ASRKF_CAND_INSIDE;
     }
     if (ctx->spill) {
         a.spill_min_D = ctx->cfg.spill_min_D;
@@ -657,6 +660,7 @@ asrkf_status asrkf_decode_step(asrkf_ctx* ctx, int32_t layer, const void* q, con
     a.Hkv = c.n_kv_heads;
     a.t = t;
     a.window_K = c.window_K;
+    a.cand_inside = c.candidates == ASRKF_CAND_INSIDE;
     a.dur_len = ctx->dur_len;
     a.tau_H = c.tau * (float)c.n_q_heads;
     a.scale_log2 = (float)(1.4426950408889634 / sqrt((double)c.head_dim));
@@ -705,6 +709,7 @@ asrkf_status asrkf_decode_step(asrkf_ctx* ctx, int32_t layer, const void* q, con
         r.Hq = c.n_q_heads;
         r.t = t;
         r.window_K = c.window_K;
+        r.cand_inside = a.cand_inside;
         r.dur_len = ctx->dur_len;
         r.history_W = c.history_W;
         r.scope_token = a.scope_token;

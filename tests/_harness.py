@@ -109,14 +109,16 @@ def oracle_levels(w, inp, seq, modes=None, with_logits=True):
 def _oracle_instance(w, inp, l, b, steps):
     K, V = inp.prompt(l, b)
     return oracle.Instance(K, V, w.window_K, w.tau, w.k_soft, capacity=w.prefill[b] + steps + 1,
-                           history_W=w.history_W, relevance_kind=w.relevance)
+                           history_W=w.history_W, relevance_kind=w.relevance,
+                           candidates=w.candidates)
 
 
 def _oracle_global(w, inp, b, steps):
     KV = [inp.prompt(l, b) for l in range(w.n_layers)]
     return oracle.GlobalInstance([k for k, _ in KV], [v for _, v in KV], w.window_K, w.tau,
                                  w.k_soft, capacity=w.prefill[b] + steps + 1,
-                                 history_W=w.history_W, relevance_kind=w.relevance)
+                                 history_W=w.history_W, relevance_kind=w.relevance,
+                                 candidates=w.candidates)
 
 
 def _record(inst, t, out, rec):
@@ -169,9 +171,17 @@ def run_oracle(w, inp, instances, modes=None, with_logits=True, steps=None, reco
     return res
 
 
+def candidate_mask(w, A, n):
+    """Which of the attended positions A the freeze loop may take, with n
+    positions after the append: outside the window of the window_K most recent
+    positions, or inside it when the workload takes candidates inside."""
+    outside = A < n - w.window_K
+    return outside if w.candidates == "outside" else ~outside
+
+
 def fix_margin_run(w, margin, relative=False, modes=None, with_logits=True, max_rounds=40):
     """Re-draw keys until every score the oracle actually compares with tau
-    (scored tokens outside the window, in the run's own active sets) keeps
+    (scored freeze candidates, in the run's own active sets) keeps
     |s - tau| >= margin (times tau when relative).  With token scope a
     token's keys are re-drawn in every layer.  Returns the attempts map."""
     attempts = {}
@@ -181,7 +191,7 @@ def fix_margin_run(w, margin, relative=False, modes=None, with_logits=True, max_
         bad = set()
 
         def on_scores(l, b, t, n, A, s):
-            near = (np.abs(s - w.tau) < lim) & (A < n - w.window_K)
+            near = (np.abs(s - w.tau) < lim) & candidate_mask(w, A, n)
             for j in A[near]:
                 for ll in (range(w.n_layers) if l is None else [l]):
                     bad.add((ll, b, int(j)))
@@ -220,7 +230,7 @@ def run_gpu(w, inp, instances, modes=None, with_logits=True, steps=None, record=
                         entropy_spike=w.entropy_spike, conf_drop=w.conf_drop,
                         wr_last_N=w.wr_last_N, dtype=w.dtype, spill_min_D=w.spill_min_D,
                         device_rows=w.device_rows, history_W=w.history_W,
-                        relevance=w.relevance, scope=w.scope)
+                        relevance=w.relevance, scope=w.scope, candidates=w.candidates)
     ctx = A.asrkf_init(cfg)
     if side_delay_us:
         A.asrkf_debug_delay_side(ctx, side_delay_us)
@@ -409,13 +419,13 @@ def compare_sampled(w, inp, instances, outs, states, record_steps):
 
 
 def score_quantile_run(w, qtl, steps=8):
-    """The qtl quantile of the scores of out-of-window tokens over the first
+    """The qtl quantile of the scores of the freeze candidates over the first
     steps of the workload with nothing frozen (tau below every score)."""
     vals = []
     wq = w.replace(tau=-1.0, steps=steps, flat_logit_steps=())
 
     def on_scores(l, b, t, n, A, s):
-        vals.append(s[A < n - w.window_K])
+        vals.append(s[candidate_mask(w, A, n)])
 
     instances = [(l, b) for l in range(w.n_layers) for b in range(w.batch)]
     run_oracle(wq, Inputs(wq), instances, with_logits=False, on_scores=on_scores)

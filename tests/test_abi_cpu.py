@@ -51,13 +51,21 @@ BASE = dict(n_layers=1, batch=1, n_q_heads=8, n_kv_heads=2, head_dim=64, max_ctx
     dict(batch=0), dict(batch=5000), dict(n_layers=0),
     dict(max_ctx=1), dict(window_K=-1), dict(k_soft=0.0), dict(tau=math.nan), dict(vocab=0),
     dict(spill_min_D=-1), dict(device_rows=64), dict(spill_min_D=2, device_rows=1),
-    dict(spill_min_D=2, device_rows=602),
+    dict(spill_min_D=2, device_rows=602), dict(candidates=2), dict(candidates=-1),
+    dict(relevance=2), dict(scope=2), dict(dtype=7),
 ])
 def test_init_rejects_invalid_config(bad):
     cfg = A.make_config(**{**BASE, **bad})
     with pytest.raises(A.AsrkfError) as e:
         A.asrkf_init(cfg)
     assert e.value.code == A._lib.EINVAL
+
+
+def test_unknown_option_names_are_refused_by_the_binding():
+    for kw in (dict(candidates="all"), dict(relevance="cosine"), dict(scope="head"),
+               dict(dtype="f16")):
+        with pytest.raises(ValueError):
+            A.make_config(**{**BASE, **kw})
 
 
 def test_null_context_is_einval():

@@ -132,3 +132,53 @@ def test_multi_head_attention(relevance, scope):
     softmax = relevance == "softmax"
     w, att = _tuned(w0, 0.5 if softmax else 0.55, relative=softmax)
     _parity(w, att)
+
+
+def _inside(**kw):
+    """Freeze candidates inside a window of 96 positions; k = 0.5 freezes a
+    token for 2 steps at its first detection, so the window's tokens come and go."""
+    args = dict(name="inside", candidates="inside", window_K=96, k_soft=0.5)
+    args.update(kw)
+    return _multi(**args)
+
+
+@pytest.mark.parametrize("relevance,scope", [("abs", "layer"), ("abs", "token"),
+                                             ("softmax", "layer"), ("softmax", "token")])
+def test_candidates_inside_window(relevance, scope):
+    """Freeze candidates taken inside the window of the K most recent positions
+    (the wording of Sec. 3.2) for both scores and both state scopes."""
+    softmax = relevance == "softmax"
+    w, att = _tuned(_inside(relevance=relevance, scope=scope), 0.5 if softmax else 0.55,
+                    relative=softmax)
+    _parity(w, att)
+
+
+@pytest.mark.parametrize("shape", [
+    dict(n_q_heads=32, n_kv_heads=8, head_dim=128, dtype="bf16"),    # one wave per token
+    dict(n_q_heads=64, n_kv_heads=8, head_dim=128, dtype="bf16"),    # two waves share a token
+    dict(n_q_heads=32, n_kv_heads=32, head_dim=128, dtype="bf16"),   # four waves share a token
+])
+def test_candidates_inside_window_layouts(shape):
+    w, att = _tuned(_inside(name="inside-layout", n_layers=2, prefill=[400, 97], steps=40,
+                            **shape), 0.55)
+    _parity(w, att)
+
+
+def test_candidates_inside_window_flag_all_hand_count():
+    """Every candidate flagged (tau = +inf), K = 32, k = 2, a 14-token prompt
+    and 255 steps: by the hand derivation each (layer, sequence) ends with the
+    tokens of relative steps 16, 18, ..., 32 frozen, 260 of 269 active."""
+    w = gen.Workload(name="inside-flag-all", seed=gen.SEED + 71, n_layers=2, batch=3,
+                     n_q_heads=32, n_kv_heads=8, head_dim=128, dtype="bf16",
+                     prefill=[14, 14, 14], steps=255, window_K=32, tau=float("inf"), k_soft=2.0,
+                     vocab=64, logit_sigma=1.0, recipe="gauss", candidates="inside")
+    inp = H.Inputs(w)
+    instances = [(l, b) for l in range(w.n_layers) for b in range(w.batch)]
+    g, _, stats = H.run_gpu(w, inp, instances, with_logits=False,
+                            record=lambda t: t in (1, 100, w.steps))
+    for key in instances:
+        last = g[key][-1]
+        assert len(last["frozen"]) == 269
+        assert int((~last["frozen"]).sum()) == 260
+        assert list(np.nonzero(last["frozen"])[0]) == sorted(269 - r for r in range(16, 33, 2))
+    assert stats[-1]["active_positions"] == 260 * len(instances)

@@ -177,3 +177,15 @@ def test_tight_device_rows_long_instance():
     peak = _resident_peak(w, H.Inputs(w))
     assert peak < w.max_ctx, peak
     _spill_parity(w.replace(device_rows=peak), H.Inputs(w))
+
+
+def test_candidates_inside_window_spill():
+    """Freeze candidates inside the window with k = 0.5: a token can freeze for
+    two steps in the step that appends it, so rows written by that step's
+    attention leave for the host store in the same step and come back."""
+    w = _flag_all(name="spill-inside", candidates="inside", k_soft=0.5, window_K=48,
+                  prefill=[200], steps=48)
+    g, o, _, stats = _spill_parity(w, H.Inputs(w))
+    assert stats[-1]["rows_from_host"] > 100
+    first = [r for r in o[(0, 0)] if r["t"] == 1][0]
+    assert first["frozen"][-1]                 # the token appended at step 1 is frozen at once
