@@ -72,6 +72,34 @@ def measured_traffic(workload, steps, warmup):
     return float(fields["traffic_bytes_per_launch"]), fields.get("layers", "all")
 
 
+def metadata_bytes(w, W, K, attended, algo_bytes, traffic, roofline):
+    """Bytes the timed steps move besides the K/V rows of attended tokens and
+    the logits (the algorithmic bytes), from the kernels' access pattern:
+    index lists (read by attention, written by compaction), freeze state (an
+    upper bound: count read and write plus U write for every attended token),
+    the compaction's scan of U over every position, q, out and the appended row
+    of every (layer, sequence), and the split-K partials (written by attention,
+    read by the combine; one workgroup per CU plus one slot per sequence).  The
+    attention kernel's measured counter excess is given beside it."""
+    import torch
+    L, B, Hq, D = w.n_layers, w.batch, w.n_q_heads, w.head_dim
+    esz = 2 if w.dtype == "bf16" else 4
+    positions = L * sum(p + t for p in w.prefill for t in range(W + 1, W + K + 1))   # n_t, summed
+    cus = torch.cuda.get_device_properties(0).multi_processor_count
+    parts = {
+        "index_lists": 8 * attended,
+        "freeze_state_upper_bound": 12 * attended,
+        "compaction_scan": 4 * positions,
+        "q_out_append": K * L * B * (Hq * D * esz + Hq * D * 4 + w.kv_bytes_per_token()),
+        "split_partials": 2 * K * L * (cus + B) * Hq * (D + 2) * 4,
+    }
+    total = sum(parts.values())
+    out = {"bytes_timed_steps": parts, "total": total, "fraction_of_algorithmic": total / algo_bytes}
+    if traffic:
+        out["attention_counter_excess"] = traffic / roofline["algorithmic_bytes_per_launch"] - 1.0
+    return out
+
+
 def cpu_baseline(w, budget_s):
     """The CPU oracle on a bounded sample: one (layer, seq) instance, the
     first steps of the run, until the time budget is spent."""
@@ -252,7 +280,7 @@ def main():
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": PEAK_HBM_GBS, "unit": "GB/s",
                      "frac": achieved / PEAK_HBM_GBS, "traffic": traffic,
                      "traffic_run_layers": traffic_layers,
-                     "kernel": "attention_kernel<bf16, D=128, G=4, Hkv=8>",
+                     "kernel": f"attention_kernel<{w.dtype}, D={D}, G={Hq // Hkv}, Hkv={Hkv}>",
                      "algorithmic_unit": f"{bytes_per_token} B per attended token-layer (K + V rows)",
                      "launches": st_timed["attn_launches"],
                      "avg_launch_us": 1e3 * st_timed["attn_kernel_ms"] / max(1, st_timed["attn_launches"]),
@@ -261,6 +289,7 @@ def main():
                      "timing": "HIP events recorded by each attention dispatch, in a replay "
                                "of the same warm-up and timed steps"},
     }
+    line["metadata"] = metadata_bytes(w, W, K, attended, algo_bytes, traffic, line["roofline"])
     if w.spill_min_D:
         row = bytes_per_token // 2                      # one K or V row
         line["spill"] = {"spill_min_D": w.spill_min_D, "rows_to_host": st["rows_to_host"],
