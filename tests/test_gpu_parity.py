@@ -194,3 +194,23 @@ def test_seeded_random_runs(case):
                      k_soft=float(np.round(rng.uniform(0.5, 3.0), 2)), vocab=64, logit_sigma=1.0,
                      recipe="gauss")
     _parity(w, H.Inputs(w))
+
+
+def _max_batch(**kw):
+    rng = np.random.default_rng(0x1024)
+    args = dict(name="max-batch", seed=gen.SEED + 81, n_layers=1, batch=1024, n_q_heads=32,
+                n_kv_heads=8, head_dim=128, dtype="bf16",
+                prefill=[int(x) for x in rng.integers(0, 61, size=1024)], steps=10,
+                window_K=8, tau=math.inf, k_soft=1.0, vocab=64, logit_sigma=1.0, recipe="gauss")
+    args.update(kw)
+    return gen.Workload(**args)
+
+
+@pytest.mark.parametrize("spill_min_D", [0, 2])
+def test_maximum_batch(spill_min_D):
+    """The largest batch the library takes (1024 sequences) with prompts of 0 to
+    60 tokens: each workgroup's range covers several sequences, most lists are
+    shorter than the per-sequence cost the planner charges, and every
+    out-of-window token is flagged each step."""
+    w = _max_batch(spill_min_D=spill_min_D)
+    _parity(w, H.Inputs(w))
