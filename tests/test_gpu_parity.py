@@ -214,3 +214,28 @@ def test_maximum_batch(spill_min_D):
     out-of-window token is flagged each step."""
     w = _max_batch(spill_min_D=spill_min_D)
     _parity(w, H.Inputs(w))
+
+
+@pytest.mark.parametrize("k_soft,window_K,forced", [
+    (2.0 ** -8, 4, True),      # d = floor(256 sqrt(c)): a token flagged once is gone for the run
+    (2.0 ** 16, 4, False),     # d = 0 for every count: nothing ever freezes
+    (1.7, 3, False),           # k not a power of two: the schedule is the exact floor for fp32 1.7
+    (0.3, 1000, False),        # the window covers every position: no candidate at all
+])
+def test_schedule_and_window_extremes(k_soft, window_K, forced):
+    """The ends of the k range the library accepts, a k that is not dyadic, and
+    a window wider than every sequence; every candidate is flagged at every
+    step (tau = +inf).  With k = 2^-8 the forced SR, WR and FR bring the
+    long-frozen tokens back."""
+    import paper_2512_11221_amd as A
+    w = gen.Workload(name="extremes", seed=gen.SEED + 91, n_layers=2, batch=3, n_q_heads=8,
+                     n_kv_heads=2, head_dim=64, dtype="f32", prefill=[50, 7, 0], steps=24,
+                     window_K=window_K, tau=math.inf, k_soft=k_soft, vocab=64, logit_sigma=1.0,
+                     recipe="gauss")
+    modes = {6: A.SR, 11: A.WR, 17: A.FR} if forced else None
+    g, o, _, stats = _parity(w, H.Inputs(w), modes=modes, with_logits=False)
+    frozen = [bool(r["frozen"].any()) for key in o for r in o[key]]
+    if k_soft >= 2.0 ** 16 or window_K >= 1000:
+        assert not any(frozen)
+    else:
+        assert any(frozen)
