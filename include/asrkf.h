@@ -152,7 +152,8 @@ asrkf_status asrkf_prefill(asrkf_ctx* ctx, int32_t layer, int32_t seq,
 /* Algorithm 1 up to the end of the freeze loop, for one layer of every
  * sequence: append the new token, attend over the active cache (Eq. 1),
  * score every attended token (Eq. 2), and freeze low-relevance tokens outside
- * the window of the window_K most recent positions (Eq. 3).
+ * the window of the window_K most recent positions (inside it with
+ * ASRKF_CAND_INSIDE) for the durations of Eq. 3.
  *   q:     device, [batch][n_q_heads][head_dim] of cfg.dtype
  *   k_new: device, [batch][n_kv_heads][head_dim] of cfg.dtype
  *   v_new: device, same layout as k_new
