@@ -101,8 +101,9 @@ def metadata_bytes(w, W, K, attended, algo_bytes, traffic, roofline):
 
 
 def cpu_baseline(w, budget_s):
-    """The CPU oracle on a bounded sample: one (layer, seq) instance, the
-    first steps of the run, until the time budget is spent."""
+    """The CPU oracle on a bounded sample: whole (layer, seq) instances in
+    order (layer 0, sequences 0, 1, ...), every step of the run, until the time
+    budget is spent."""
     import numpy as np
     import oracle
     from synth import gen
@@ -111,31 +112,36 @@ def cpu_baseline(w, budget_s):
         threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
     except Exception:
         threads = 1
-    P = w.prefill[0]
-    K, V = gen.kv_rows(w, 0, 0, 0, P + w.steps)
-    inst = oracle.Instance(K[:P], V[:P], w.window_K, w.tau, w.k_soft, capacity=P + w.steps + 1,
-                           history_W=w.history_W, relevance_kind=w.relevance,
-                           candidates=w.candidates)
-    attended, spent, steps = 0, 0.0, 0
-    for t in range(1, w.steps + 1):
-        q = gen.q_row(w, 0, 0, t)
-        t0 = time.perf_counter()
-        rec = inst.step(q, K[P + t - 1], V[P + t - 1])
-        spent += time.perf_counter() - t0
-        attended += len(rec.active)
-        steps = t
+    attended, spent, inst_steps, done = 0, 0.0, 0, []
+    order = [(l, b) for l in range(w.n_layers) for b in range(w.batch)]
+    for (l, b) in order:
+        P = w.prefill[b]
+        K, V = gen.kv_rows(w, l, b, 0, P + w.steps)
+        inst = oracle.Instance(K[:P], V[:P], w.window_K, w.tau, w.k_soft,
+                               capacity=P + w.steps + 1, history_W=w.history_W,
+                               relevance_kind=w.relevance, candidates=w.candidates)
+        for t in range(1, w.steps + 1):
+            q = gen.q_row(w, l, b, t)
+            t0 = time.perf_counter()
+            rec = inst.step(q, K[P + t - 1], V[P + t - 1])
+            spent += time.perf_counter() - t0
+            attended += len(rec.active)
+            inst_steps += 1
+            if spent >= budget_s:
+                break
+        done.append((l, b, t))
         if spent >= budget_s:
             break
-    instances = w.n_layers * w.batch
+    instances = len(order)
+    what = ", ".join(f"layer {l} seq {b} steps 1..{t}" for l, b, t in done)
     return {"value": attended / spent, "unit": "active KV token-layers/s", "cores": threads,
             "kind": "oracle",
-            "sample": f"layer 0, sequence 0 of {w.name}: steps 1..{steps} "
-                      f"({attended} attended token-layers in {spent:.1f} s); "
+            "sample": f"{w.name}: {what} ({attended} attended token-layers in {spent:.1f} s); "
                       f"the full step has {instances} such instances",
             "cpu_count": os.cpu_count(),
             "affinity": len(os.sched_getaffinity(0)) if hasattr(os, "sched_getaffinity") else None,
-            "ms_per_step_extrapolated": 1e3 * spent / steps * instances,
-            "extrapolation": f"the sample's mean time per step x {instances} instances"}
+            "ms_per_step_extrapolated": 1e3 * spent / inst_steps * instances,
+            "extrapolation": f"the sample's mean time per instance step x {instances} instances"}
 
 
 def main():
