@@ -34,6 +34,21 @@ def test_schedule_table_matches_oracle(k):
     np.testing.assert_array_equal(tab, ref)
 
 
+def test_schedule_table_extremes_and_random_k():
+    """The ends of the accepted k range and 24 seeded log-uniform k values,
+    each rounded to float32 (the value the library sees): the table is the
+    exact floor of sqrt(c) / k for every count."""
+    rng = np.random.default_rng(0x5CED)
+    ks = [2.0 ** -8, 2.0 ** 16, 1.7, 0.1, 1.0 / 3.0]
+    ks += list(2.0 ** rng.uniform(-8, 16, size=24))
+    for k in ks:
+        k32 = float(np.float32(k))
+        # the oracle searches d one step at a time: keep its work near 3e5 steps per k
+        n = int(min(5000, max(100, (4.5e5 * k32) ** (2.0 / 3.0))))
+        np.testing.assert_array_equal(A.asrkf_schedule_table(k32, n), oracle.duration_table(n - 1, k32),
+                                      err_msg=f"k = {k32!r}")
+
+
 def test_schedule_table_rejects_bad_k():
     for k in (0.0, -1.0, math.inf, math.nan, 1e-5, 1e6):
         with pytest.raises(A.AsrkfError):
