@@ -1,11 +1,11 @@
 // Entropy of the next-token distribution and the recovery ladder (Sec. 3.6).
 //
-// kEntropySplit workgroups per sequence, one pass over the V logits.  Each
+// a.split workgroups per sequence, one pass over the V logits.  Each
 // thread forms (m, S, T) with S = sum e^(x-m) and T = sum e^(x-m) (x-m) over
 // its logits (all loads of a round in flight together, the round's maximum
 // first); the triples are merged across the block and stored.  The last
-// block of a sequence to finish (a per-sequence ticket) merges the stored
-// triples in block order and forms
+// block of a sequence to finish (a per-sequence ticket) loads the stored
+// triples, one per lane, merges them in a fixed lane tree and forms
 //     H = ln S - T / S          (nats, softmax at temperature 1)
 //     p_max = 1 / S,
 // then updates the sequence's escalation count (one level per consecutive
@@ -26,9 +26,10 @@ struct Triple {
 __device__ __forceinline__ Triple merge(const Triple& a, const Triple& b) {
     if (b.S == 0.f) return a;
     if (a.S == 0.f) return b;
+    constexpr float kLog2e = 1.4426950408889634f;
     const float m = fmaxf(a.m, b.m);
     const float da = a.m - m, db = b.m - m;
-    const float ea = expf(da), eb = expf(db);
+    const float ea = __builtin_amdgcn_exp2f(da * kLog2e), eb = __builtin_amdgcn_exp2f(db * kLog2e);
     Triple r;
     r.m = m;
     r.S = ea * a.S + eb * b.S;
@@ -67,7 +68,7 @@ entropy_kernel(EntropyArgs a) {
     Triple acc{-INFINITY, 0.f, 0.f};
     if (((reinterpret_cast<uintptr_t>(x) & 15) == 0) && (a.V % 4 == 0)) {
         const int n4 = a.V / 4;
-        const int i0 = (int)((int64_t)sp * n4 / kEntropySplit), i1 = (int)((int64_t)(sp + 1) * n4 / kEntropySplit);
+        const int i0 = (int)((int64_t)sp * n4 / a.split), i1 = (int)((int64_t)(sp + 1) * n4 / a.split);
         // all of a round's loads are issued before any of them is used
         for (int base = i0; base < i1; base += kThreads * kVec) {
             float v[4 * kVec];
@@ -85,7 +86,7 @@ entropy_kernel(EntropyArgs a) {
             acc = merge(acc, triple_of(v, ok));
         }
     } else {
-        const int i0 = (int)((int64_t)sp * a.V / kEntropySplit), i1 = (int)((int64_t)(sp + 1) * a.V / kEntropySplit);
+        const int i0 = (int)((int64_t)sp * a.V / a.split), i1 = (int)((int64_t)(sp + 1) * a.V / a.split);
         for (int i = i0 + threadIdx.x; i < i1; i += kThreads) {
             const float v[1] = {x[i]};
             const bool ok[1] = {true};
@@ -101,7 +102,7 @@ entropy_kernel(EntropyArgs a) {
     if (threadIdx.x == 0) {
         Triple r = part[0];
         for (int w = 1; w < kThreads / 64; ++w) r = merge(r, part[w]);
-        float* dst = a.partial + ((size_t)b * kEntropySplit + sp) * 3;
+        float* dst = a.partial + ((size_t)b * a.split + sp) * 3;
         __hip_atomic_store(dst, r.m, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         __hip_atomic_store(dst + 1, r.S, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         __hip_atomic_store(dst + 2, r.T, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -109,19 +110,26 @@ entropy_kernel(EntropyArgs a) {
         // so no cache-wide write-back is needed
         __builtin_amdgcn_s_waitcnt(0);
         last = (__hip_atomic_fetch_add(a.ticket + b, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)
-                == kEntropySplit - 1);
+                == a.split - 1);
     }
     __syncthreads();
-    if (!last || threadIdx.x != 0) return;
-    // the other blocks' triples, read at device scope (they may sit in another XCD's L2),
-    // all loads issued before the fixed-order merge
-    float* src = a.partial + (size_t)b * kEntropySplit * 3;
-    float tv[3 * kEntropySplit];
-#pragma unroll
-    for (int k = 0; k < 3 * kEntropySplit; ++k)
-        tv[k] = __hip_atomic_load(src + k, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    Triple r{tv[0], tv[1], tv[2]};
-    for (int k = 1; k < kEntropySplit; ++k) r = merge(r, Triple{tv[3 * k], tv[3 * k + 1], tv[3 * k + 2]});
+    if (!last || threadIdx.x >= 64) return;
+    // the blocks' triples, one per lane, read at device scope (they may sit in
+    // another XCD's L2); merged in a fixed lane tree, so every run rounds alike
+    static_assert(kEntropySplitMax <= 64, "one triple per lane");
+    const float* src = a.partial + (size_t)b * a.split * 3;
+    const int k = threadIdx.x;
+    Triple r{-INFINITY, 0.f, 0.f};
+    if (k < a.split) {
+        r.m = __hip_atomic_load(src + 3 * k, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        r.S = __hip_atomic_load(src + 3 * k + 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        r.T = __hip_atomic_load(src + 3 * k + 2, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
+    for (int o = 1; o < 64; o <<= 1) {
+        Triple other{__shfl_xor(r.m, o), __shfl_xor(r.S, o), __shfl_xor(r.T, o)};
+        r = (k & o) ? merge(other, r) : merge(r, other);
+    }
+    if (k != 0) return;
     a.ticket[b] = 0;                           // ready for the next step
     const float H = logf(r.S) - r.T / r.S;
     const float pmax = 1.f / r.S;
@@ -144,7 +152,7 @@ entropy_kernel(EntropyArgs a) {
 }  // namespace
 
 hipError_t launch_entropy(const EntropyArgs& a, hipStream_t s) {
-    hipLaunchKernelGGL(entropy_kernel, dim3(kEntropySplit, a.B), dim3(kThreads), 0, s, a);
+    hipLaunchKernelGGL(entropy_kernel, dim3(a.split, a.B), dim3(kThreads), 0, s, a);
     return hipGetLastError();
 }
 

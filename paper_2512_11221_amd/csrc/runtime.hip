@@ -102,7 +102,7 @@ struct asrkf_ctx {
     float* part_acc = nullptr;
     float* part_ml = nullptr;
     int32_t* slot_info = nullptr;   // [2B]: first slot, end slot per sequence
-    float* ent_partial = nullptr;   // [B][kEntropySplit][3]
+    float* ent_partial = nullptr;   // [B][kEntropySplitMax][3]
     int32_t* ent_ticket = nullptr;  // [B]
     unsigned long long* counters = nullptr;   // [0] listed_total, [1..3] recoveries, [5] rr,
                                               // [8] rows to host, [9] rows from host, [10] released
@@ -364,7 +364,7 @@ asrkf_status asrkf_init(const asrkf_config* cfg, asrkf_ctx** out) {
     ALLOC(part_acc, (size_t)ctx->n_slots * c.n_q_heads * c.head_dim * 4);
     ALLOC(part_ml, (size_t)ctx->n_slots * c.n_q_heads * 2 * 4);
     ALLOC(slot_info, (size_t)c.batch * 2 * 4);
-    ALLOC(ent_partial, (size_t)c.batch * kEntropySplit * 3 * 4);
+    ALLOC(ent_partial, (size_t)c.batch * kEntropySplitMax * 3 * 4);
     ALLOC(ent_ticket, (size_t)c.batch * 4);
     ALLOC(counters, kCounters * sizeof(unsigned long long));
     if (ctx->spill) {
@@ -740,6 +740,7 @@ asrkf_status asrkf_restore(asrkf_ctx* ctx, const float* logits, int32_t mode, vo
         EntropyArgs e{};
         e.logits = logits;
         e.partial = ctx->ent_partial;
+        e.split = entropy_split(c.batch);
         e.ticket = ctx->ent_ticket;
         e.V = c.vocab;
         e.B = c.batch;
