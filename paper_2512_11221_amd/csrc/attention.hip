@@ -761,18 +761,21 @@ attention_kernel(AttnArgs a) {
 }
 
 // Split combine.  A block owns 64 dims of one query head of one sequence;
-// its 4 slot groups each fold every 4th partial slot into a running
-// (max, sum, acc) in one pass (all loads of a group issued together), and
-// the groups' states are folded in a fixed order:
+// its GROUPS slot groups each fold every GROUPS-th partial slot into a running
+// (max, sum, acc) in passes of kSlotUnroll slots (all loads of a pass issued
+// together), and the groups' states are folded in a fixed order:
 //   out[b][h][d] = sum_s 2^(m_s - M) acc_s[d] / sum_s 2^(m_s - M) l_s.
-constexpr int kFinishThreads = 256;
+// The launch sizes GROUPS to the slots a sequence has, so that a sequence's
+// partials take few dependent passes (one sequence over the whole device has
+// about 257 slots, eight sequences about 33, sixty-four about 5).
 constexpr int kFinishDims = 64;
-constexpr int kSlotGroups = kFinishThreads / kFinishDims;
 constexpr int kSlotUnroll = 8;
 
-__global__ void __launch_bounds__(kFinishThreads)
+template <int GROUPS>
+__global__ void __launch_bounds__(kFinishDims * GROUPS)
 finish_kernel(FinishArgs a, int D) {
-    __shared__ float sm[kFinishThreads], sl[kFinishThreads], sa[kFinishThreads];
+    constexpr int kThreads = kFinishDims * GROUPS;
+    __shared__ float sm[kThreads], sl[kThreads], sa[kThreads];
     const int per_head = D / kFinishDims;
     const int bh = blockIdx.x / per_head;                 // b * Hq + h
     const int d = (blockIdx.x % per_head) * kFinishDims + threadIdx.x % kFinishDims;
@@ -780,11 +783,11 @@ finish_kernel(FinishArgs a, int D) {
     const int b = bh / a.Hq, h = bh % a.Hq;
     const int s0 = a.slot_first[b], s1 = a.slot_end[b];
     float M = -INFINITY, L = 0.f, acc = 0.f;
-    for (int k = s0 + grp; k < s1; k += kSlotGroups * kSlotUnroll) {
+    for (int k = s0 + grp; k < s1; k += GROUPS * kSlotUnroll) {
         float mk[kSlotUnroll], lk[kSlotUnroll], ak[kSlotUnroll];
 #pragma unroll
         for (int u = 0; u < kSlotUnroll; ++u) {
-            const int ks = min(k + u * kSlotGroups, s1 - 1);
+            const int ks = min(k + u * GROUPS, s1 - 1);
             const size_t head = (size_t)ks * a.Hq + h;
             mk[u] = a.part_ml[head * 2];
             lk[u] = a.part_ml[head * 2 + 1];
@@ -793,13 +796,13 @@ finish_kernel(FinishArgs a, int D) {
         float Mn = M;
 #pragma unroll
         for (int u = 0; u < kSlotUnroll; ++u)
-            if (k + u * kSlotGroups < s1) Mn = fmaxf(Mn, mk[u]);
+            if (k + u * GROUPS < s1) Mn = fmaxf(Mn, mk[u]);
         const float sc = (M == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(M - Mn);
         L *= sc;
         acc *= sc;
 #pragma unroll
         for (int u = 0; u < kSlotUnroll; ++u) {
-            if (k + u * kSlotGroups < s1) {
+            if (k + u * GROUPS < s1) {
                 const float wgt = __builtin_amdgcn_exp2f(mk[u] - Mn);
                 L = fmaf(wgt, lk[u], L);
                 acc = fmaf(wgt, ak[u], acc);
@@ -807,27 +810,31 @@ finish_kernel(FinishArgs a, int D) {
         }
         M = Mn;
     }
-    sm[threadIdx.x] = M;
-    sl[threadIdx.x] = L;
-    sa[threadIdx.x] = acc;
-    __syncthreads();
-    if (grp == 0) {
+    if constexpr (GROUPS > 1) {
+        sm[threadIdx.x] = M;
+        sl[threadIdx.x] = L;
+        sa[threadIdx.x] = acc;
+        __syncthreads();
+        if (grp != 0) return;
         float Mt = -INFINITY;
 #pragma unroll
-        for (int k = 0; k < kSlotGroups; ++k) Mt = fmaxf(Mt, sm[k * kFinishDims + threadIdx.x]);
+        for (int k = 0; k < GROUPS; ++k) Mt = fmaxf(Mt, sm[k * kFinishDims + threadIdx.x]);
         float o = 0.f, lt = 0.f;
 #pragma unroll
-        for (int k = 0; k < kSlotGroups; ++k) {
+        for (int k = 0; k < GROUPS; ++k) {
             const float mk = sm[k * kFinishDims + threadIdx.x];
             const float wgt = (mk == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(mk - Mt);
             o = fmaf(wgt, sa[k * kFinishDims + threadIdx.x], o);
             lt = fmaf(wgt, sl[k * kFinishDims + threadIdx.x], lt);
         }
-        a.out[(size_t)bh * D + d] = o / lt;
-        if (a.norm && threadIdx.x == 0 && blockIdx.x % per_head == 0) {
-            a.norm[(size_t)bh * 2] = Mt;
-            a.norm[(size_t)bh * 2 + 1] = lt;
-        }
+        M = Mt;
+        L = lt;
+        acc = o;
+    }
+    a.out[(size_t)bh * D + d] = acc / L;
+    if (a.norm && threadIdx.x == 0 && blockIdx.x % per_head == 0) {
+        a.norm[(size_t)bh * 2] = M;
+        a.norm[(size_t)bh * 2 + 1] = L;
     }
 }
 
@@ -951,10 +958,15 @@ hipError_t attention_occupancy(const AttnArgs& a, int dtype_bf16, int head_dim, 
     return dispatch(a, dtype_bf16, head_dim, group, Launch{0, nullptr, nullptr, nullptr, blocks_per_cu});
 }
 
-hipError_t launch_finish(const FinishArgs& a, int head_dim, hipStream_t s) {
+hipError_t launch_finish(const FinishArgs& a, int head_dim, int slots_per_seq, hipStream_t s) {
     if (head_dim % kFinishDims) return hipErrorInvalidValue;
     const dim3 grid(a.B * a.Hq * (head_dim / kFinishDims));
-    hipLaunchKernelGGL(finish_kernel, grid, dim3(kFinishThreads), 0, s, a, head_dim);
+    if (slots_per_seq > 8 * kSlotUnroll)
+        hipLaunchKernelGGL(finish_kernel<16>, grid, dim3(kFinishDims * 16), 0, s, a, head_dim);
+    else if (slots_per_seq > kSlotUnroll)
+        hipLaunchKernelGGL(finish_kernel<4>, grid, dim3(kFinishDims * 4), 0, s, a, head_dim);
+    else
+        hipLaunchKernelGGL(finish_kernel<1>, grid, dim3(kFinishDims), 0, s, a, head_dim);
     return hipGetLastError();
 }
 

@@ -211,7 +211,8 @@ hipError_t launch_attention(const AttnArgs& a, int dtype_bf16, int head_dim, int
                             int grid, hipStream_t s, hipEvent_t start, hipEvent_t stop);
 hipError_t attention_occupancy(const AttnArgs& a, int dtype_bf16, int head_dim, int group,
                                int* blocks_per_cu);
-hipError_t launch_finish(const FinishArgs& a, int head_dim, hipStream_t s);
+// slots_per_seq: about how many partial slots a sequence has (grid / B + 1).
+hipError_t launch_finish(const FinishArgs& a, int head_dim, int slots_per_seq, hipStream_t s);
 hipError_t launch_compact(const CompactArgs& a, int n_instances, hipStream_t s);
 // Segments per instance (and their length) for the rebuild; 1 = one workgroup per instance.
 int compact_segments(int n_instances, int cap, int* seg_len);

@@ -690,7 +690,7 @@ asrkf_status asrkf_decode_step(asrkf_ctx* ctx, int32_t layer, const void* q, con
     f.norm = ctx->norm;
     f.B = c.batch;
     f.Hq = c.n_q_heads;
-    HIP_OK(ctx, launch_finish(f, c.head_dim, s));
+    HIP_OK(ctx, launch_finish(f, c.head_dim, ctx->grid / c.batch + 1, s));
     if (c.relevance == ASRKF_REL_SOFTMAX) {
         RelevanceArgs r{};
         r.xlog = ctx->xlog;
