@@ -239,3 +239,26 @@ def test_schedule_and_window_extremes(k_soft, window_K, forced):
         assert not any(frozen)
     else:
         assert any(frozen)
+
+
+@pytest.mark.parametrize("batch", [20, 40, 200])
+def test_entropy_and_combine_across_batch_sizes(batch):
+    """Batch sizes at which the launches take other shapes: the entropy pass
+    splits a sequence's 128256 logits over 16, 8 or 4 workgroups (32 below
+    batch 17), and the split combine folds a sequence's partial slots with 4 or
+    1 slot groups.  Entropy and the confidence of every sequence at every step
+    against the oracle; states bit-exact and outputs in tolerance."""
+    rng = np.random.default_rng(0x5EED + batch)
+    w = gen.Workload(name=f"batch-{batch}", seed=gen.SEED + 101 + batch, n_layers=1, batch=batch,
+                     n_q_heads=8, n_kv_heads=2, head_dim=64, dtype="f32",
+                     prefill=[int(x) for x in rng.integers(1, 90, size=batch)], steps=3,
+                     window_K=8, tau=math.inf, k_soft=1.0, vocab=128256, logit_sigma=3.0,
+                     recipe="gauss")
+    inp = H.Inputs(w)
+    _, _, mon, _ = _parity(w, inp)
+    for b in range(batch):
+        for t in range(1, w.steps + 1):
+            e, pmax = H.oracle.entropy(inp.logits(b, t))
+            m = mon[b][t - 1]
+            assert abs(m["entropy"] - e) <= H.ENTROPY_TOL, (b, t, m["entropy"], e)
+            assert abs(m["pmax"] - pmax) <= 1e-6 + 1e-4 * pmax, (b, t, m["pmax"], pmax)
