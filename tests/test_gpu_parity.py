@@ -262,3 +262,27 @@ def test_entropy_and_combine_across_batch_sizes(batch):
             m = mon[b][t - 1]
             assert abs(m["entropy"] - e) <= H.ENTROPY_TOL, (b, t, m["entropy"], e)
             assert abs(m["pmax"] - pmax) <= 1e-6 + 1e-4 * pmax, (b, t, m["pmax"], pmax)
+
+
+@pytest.mark.parametrize("batch,vocab", [(3, 1), (3, 7), (40, 7), (3, 1001), (40, 1001)])
+def test_entropy_small_and_unaligned_vocab(batch, vocab):
+    """Vocabularies that take the entropy pass's element-wise path (not a
+    multiple of four logits), fewer logits than the workgroups a sequence is
+    split over (so some of them fold nothing), and the one-logit distribution
+    (entropy 0, confidence 1)."""
+    rng = np.random.default_rng(0xE17 + vocab + batch)
+    w = gen.Workload(name=f"vocab-{vocab}", seed=gen.SEED + 131 + vocab + batch, n_layers=1,
+                     batch=batch, n_q_heads=8, n_kv_heads=2, head_dim=64, dtype="f32",
+                     prefill=[int(x) for x in rng.integers(1, 40, size=batch)], steps=2,
+                     window_K=8, tau=math.inf, k_soft=1.0, vocab=vocab, logit_sigma=3.0,
+                     recipe="gauss")
+    inp = H.Inputs(w)
+    _, _, mon, _ = _parity(w, inp)
+    for b in range(batch):
+        for t in range(1, w.steps + 1):
+            e, pmax = H.oracle.entropy(inp.logits(b, t))
+            m = mon[b][t - 1]
+            assert abs(m["entropy"] - e) <= H.ENTROPY_TOL, (b, t, m["entropy"], e)
+            assert abs(m["pmax"] - pmax) <= 1e-6 + 1e-4 * pmax, (b, t, m["pmax"], pmax)
+            if vocab == 1:
+                assert m["entropy"] == 0.0 and m["pmax"] == 1.0
