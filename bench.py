@@ -45,7 +45,33 @@ def parse():
                     help="run only the first N layers of the workload (counter runs); 0 = all")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",
                     help="after the run, one plain device copy of BYTES (counter calibration)")
+    ap.add_argument("--summarize-counters", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
+                    help="print the HBM traffic per attention launch from two rocprofv3 --pmc "
+                         "runs (FETCH_SIZE, WRITE_SIZE) made with --copy-calibration; no GPU work")
     return ap.parse_args()
+
+
+def summarize_counters(fetch_dir, write_dir, timed, copy_bytes):
+    """HBM bytes per attention launch from two rocprofv3 counter runs: the mean
+    FETCH_SIZE and WRITE_SIZE (KiB per dispatch) of the last `timed` attention
+    dispatches, each scaled by what the same counter read for the run's final
+    plain device copy of `copy_bytes` bytes."""
+    import csv
+    import glob
+    out = {}
+    for d, counter in ((fetch_dir, "FETCH_SIZE"), (write_dir, "WRITE_SIZE")):
+        path = glob.glob(os.path.join(d, "**", "*counter_collection.csv"), recursive=True)[0]
+        rows = [r for r in csv.DictReader(open(path)) if r["Counter_Name"] == counter]
+        rows.sort(key=lambda r: int(r["Dispatch_Id"]))
+        att = [float(r["Counter_Value"]) for r in rows if "attention_kernel" in r["Kernel_Name"]][-timed:]
+        copy_kib = [float(r["Counter_Value"]) for r in rows if "copyBuffer" in r["Kernel_Name"]][-1]
+        factor = copy_bytes / (copy_kib * 1024)
+        mean = sum(att) / len(att)
+        out[counter] = {"attention_kib_raw": mean, "copy_kib_raw": copy_kib, "factor": factor,
+                        "bytes_per_launch": mean * 1024 * factor, "launches": len(att)}
+    out["traffic_bytes_per_launch"] = round(out["FETCH_SIZE"]["bytes_per_launch"]
+                                            + out["WRITE_SIZE"]["bytes_per_launch"])
+    return out
 
 
 TRAFFIC_SUMMARY = os.path.join(ROOT, "profiles", "attention_traffic_llama3-8b-32layer.md")
@@ -146,6 +172,10 @@ def cpu_baseline(w, budget_s):
 
 def main():
     args = parse()
+    if args.summarize_counters:
+        print(json.dumps(summarize_counters(*args.summarize_counters, args.steps,
+                                            args.copy_calibration or (1 << 30)), indent=1))
+        return
     if args.gpus != 1:
         print(f"bench.py measures one GPU only: the library has no multi-GPU path "
               f"(asked for --gpus {args.gpus}).", file=sys.stderr)
