@@ -45,17 +45,20 @@ def parse():
                     help="run only the first N layers of the workload (counter runs); 0 = all")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",
                     help="after the run, one plain device copy of BYTES (counter calibration)")
-    ap.add_argument("--summarize-counters", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
+    ap.add_argument("--summarize-counters", nargs=3, metavar=("FETCH_DIR", "WRITE_DIR", "BENCH_LOG"),
                     help="print the HBM traffic per attention launch from two rocprofv3 --pmc "
-                         "runs (FETCH_SIZE, WRITE_SIZE) made with --copy-calibration; no GPU work")
+                         "runs (FETCH_SIZE, WRITE_SIZE) made with --copy-calibration, and its "
+                         "ratio to the algorithmic bytes in the JSON line that the FETCH_SIZE "
+                         "run printed (BENCH_LOG); no GPU work")
     return ap.parse_args()
 
 
-def summarize_counters(fetch_dir, write_dir, timed, copy_bytes):
+def summarize_counters(fetch_dir, write_dir, bench_log, timed, copy_bytes):
     """HBM bytes per attention launch from two rocprofv3 counter runs: the mean
     FETCH_SIZE and WRITE_SIZE (KiB per dispatch) of the last `timed` attention
     dispatches, each scaled by what the same counter read for the run's final
-    plain device copy of `copy_bytes` bytes."""
+    plain device copy of `copy_bytes` bytes; and their ratio to the algorithmic
+    bytes per launch of the same window (the bench line in bench_log)."""
     import csv
     import glob
     out = {}
@@ -71,6 +74,10 @@ def summarize_counters(fetch_dir, write_dir, timed, copy_bytes):
                         "bytes_per_launch": mean * 1024 * factor, "launches": len(att)}
     out["traffic_bytes_per_launch"] = round(out["FETCH_SIZE"]["bytes_per_launch"]
                                             + out["WRITE_SIZE"]["bytes_per_launch"])
+    line = next(json.loads(x) for x in open(bench_log) if x.startswith("{"))
+    algo = line["roofline"]["algorithmic_bytes_per_launch"]
+    out["algorithmic_bytes_per_launch"] = algo
+    out["traffic_per_algorithmic_byte"] = out["traffic_bytes_per_launch"] / algo
     return out
 
 
@@ -78,12 +85,14 @@ TRAFFIC_SUMMARY = os.path.join(ROOT, "profiles", "attention_traffic_llama3-8b-32
 ATTENTION_SOURCE = os.path.join(ROOT, "paper_2512_11221_amd", "csrc", "attention.hip")
 
 
-def measured_traffic(workload, steps, warmup):
-    """HBM bytes per attention launch from the committed rocprofv3 counter
-    summary, if it was taken on this workload, these steps and this kernel
-    source; otherwise None.  The summary may come from a run of the first
-    layer only: every attention launch covers one layer of the whole batch,
-    so the launches of that run have the same shape as the full run's."""
+def measured_traffic(workload):
+    """HBM bytes per algorithmic byte of the attention kernel, from the
+    committed rocprofv3 counter summary, if it was taken on this workload's
+    shape and this kernel source; otherwise None.  The counter runs measure
+    FETCH_SIZE + WRITE_SIZE per launch over a window of steps; dividing by the
+    algorithmic bytes of the same launches gives a ratio that carries to any
+    window of the same workload (the kernel reads 4096 B per attended
+    token-layer plus a small fixed part per launch)."""
     import hashlib
     import re
     if not os.path.exists(TRAFFIC_SUMMARY):
@@ -92,10 +101,9 @@ def measured_traffic(workload, steps, warmup):
     fields = dict(re.findall(r"^- (\w+): `([^`]*)`", text, flags=re.M))
     with open(ATTENTION_SOURCE, "rb") as f:
         sha = hashlib.sha256(f.read()).hexdigest()
-    if (fields.get("workload") != workload or fields.get("attention_source_sha256") != sha
-            or fields.get("steps") != str(steps) or fields.get("warmup") != str(warmup)):
+    if fields.get("workload") != workload or fields.get("attention_source_sha256") != sha:
         return None
-    return float(fields["traffic_bytes_per_launch"]), fields.get("layers", "all")
+    return float(fields["traffic_per_algorithmic_byte"]), fields
 
 
 def metadata_bytes(w, W, K, attended, algo_bytes, traffic, roofline):
@@ -123,6 +131,41 @@ def metadata_bytes(w, W, K, attended, algo_bytes, traffic, roofline):
     out = {"bytes_timed_steps": parts, "total": total, "fraction_of_algorithmic": total / algo_bytes}
     if traffic:
         out["attention_counter_excess"] = traffic / roofline["algorithmic_bytes_per_launch"] - 1.0
+    return out
+
+
+def regimes(w, W, K, series, bytes_per_token):
+    """The timed steps split by regime.  Every prompt token starts uncounted,
+    so the freezable cohort moves in lockstep: at a dense step (nearly) every
+    position attends, at a sparse step (the method's operating point) the
+    frozen cohort is out.  A step counts as dense when at least 90 % of the
+    positions attend.
+    Per regime: attended token-layers per attention launch, the launches'
+    mean duration (the replay's dispatch events), that kernel's fraction of
+    the HBM peak, and the whole step's fraction (algorithmic bytes, the
+    logits included, over the step's GPU time in the replay)."""
+    L, B = w.n_layers, w.batch
+    out = {}
+    for name in ("dense", "sparse"):
+        idx = []
+        for i, t in enumerate(range(W + 1, W + K + 1)):
+            every = L * sum(p + t for p in w.prefill)          # positions n_t of every instance
+            if (series["attended"][i] >= 0.9 * every) == (name == "dense"):
+                idx.append(i)
+        if not idx:
+            out[name] = None
+            continue
+        tokens = sum(series["attended"][i] for i in idx)
+        attn_ms = sum(series["attn_ms"][i] for i in idx)
+        step_ms = sum(series["gpu_ms"][i] for i in idx)
+        launch_us = 1e3 * attn_ms / (L * len(idx))
+        achieved = bytes_per_token * tokens / (attn_ms / 1e3) / 1e9
+        step_bytes = bytes_per_token * tokens + 4 * w.vocab * B * len(idx)
+        out[name] = {"steps": len(idx), "token_layers_per_launch": tokens / (L * len(idx)),
+                     "avg_launch_us": launch_us, "achieved": achieved,
+                     "frac": achieved / PEAK_HBM_GBS,
+                     "step_ms": step_ms / len(idx),
+                     "step_frac": step_bytes / (step_ms / 1e3) / 1e9 / PEAK_HBM_GBS}
     return out
 
 
@@ -240,7 +283,7 @@ def main():
         A.asrkf_stats_reset(ctx)
         A.asrkf_set_timing(ctx, timing)
         torch.cuda.synchronize()
-        series = {"gpu_ms": [], "attended": []}
+        series = {"gpu_ms": [], "attended": [], "attn_ms": []}
         t0 = time.perf_counter()
         for t in range(W + 1, W + K + 1):
             if timing:
@@ -252,7 +295,9 @@ def main():
                 e1.record()
                 e1.synchronize()
                 series["gpu_ms"].append(round(e0.elapsed_time(e1), 4))
-                series["attended"].append(A.asrkf_stats(ctx)["attended_total"])
+                st_t = A.asrkf_stats(ctx)
+                series["attended"].append(st_t["attended_total"])
+                series["attn_ms"].append(st_t["attn_kernel_ms"])
             else:
                 step(t)
         torch.cuda.synchronize()
@@ -260,8 +305,10 @@ def main():
         st = A.asrkf_stats(ctx)
         A.asrkf_destroy(ctx)
         if timing:
-            cum = series["attended"]
-            series["attended"] = [c - p for c, p in zip(cum, [0] + cum[:-1])]
+            for key in ("attended", "attn_ms"):
+                cum = series[key]
+                series[key] = [c - p for c, p in zip(cum, [0] + cum[:-1])]
+            series["attn_ms"] = [round(x, 5) for x in series["attn_ms"]]
         return elapsed, st, series
 
     # The step rate comes from a pass without instrumentation; the attention
@@ -279,8 +326,9 @@ def main():
     achieved = bytes_per_token * attended / attn_s / 1e9
     default_path = (w.relevance == "abs" and w.scope == "layer" and not w.history_W
                     and not w.spill_min_D and w.candidates == "outside")
-    traffic = measured_traffic(w.name, K, W) if default_path else None
-    traffic, traffic_layers = traffic if traffic else (None, None)
+    ratio = measured_traffic(w.name) if default_path else None
+    launches = max(1, st_timed["attn_launches"])
+    traffic = ratio[0] * bytes_per_token * attended / launches if ratio else None
     if args.copy_calibration > 0:
         src = torch.empty(args.copy_calibration, dtype=torch.uint8, device="cuda")
         dst = torch.empty_like(src)
@@ -315,7 +363,12 @@ def main():
         "step_series": series,
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": PEAK_HBM_GBS, "unit": "GB/s",
                      "frac": achieved / PEAK_HBM_GBS, "traffic": traffic,
-                     "traffic_run_layers": traffic_layers,
+                     "traffic_basis": (f"HBM bytes per algorithmic byte ({ratio[0]:.4f}) from two "
+                                       f"rocprofv3 counter runs (FETCH_SIZE, WRITE_SIZE, copy-"
+                                       f"calibrated) of this kernel source on this workload "
+                                       f"({ratio[1].get('layers', 'all')} layer(s), "
+                                       f"{ratio[1].get('steps')} timed steps), times this run's "
+                                       f"algorithmic bytes per launch") if ratio else None,
                      "kernel": f"attention_kernel<{w.dtype}, D={D}, G={Hq // Hkv}, Hkv={Hkv}>",
                      "algorithmic_unit": f"{bytes_per_token} B per attended token-layer (K + V rows)",
                      "launches": st_timed["attn_launches"],
@@ -325,6 +378,7 @@ def main():
                      "timing": "HIP events recorded by each attention dispatch, in a replay "
                                "of the same warm-up and timed steps"},
     }
+    line["roofline"].update(regimes(w, W, K, series, bytes_per_token))
     line["metadata"] = metadata_bytes(w, W, K, attended, algo_bytes, traffic, line["roofline"])
     if w.spill_min_D:
         row = bytes_per_token // 2                      # one K or V row

@@ -22,7 +22,12 @@
  *    buffer it passes and keeps it valid until the work queued on `stream`
  *    has finished.  The library owns its cache, state, scratch and events.
  *  - `stream` is a hipStream_t passed as void*; NULL is the default stream.
- *    Calls marked "asynchronous" only queue work on that stream.
+ *    Calls marked "asynchronous" only queue work on that stream.  Successive
+ *    calls on one context may use different streams: a call on another
+ *    stream than the context's previous call first makes its stream wait for
+ *    the work that call queued (the context's cache, states and scratch are
+ *    shared by all calls).  Calls marked "waits" synchronize only the
+ *    context's own streams, not the whole device.
  *  - On any HIP runtime error the context is poisoned: that call returns
  *    ASRKF_EHIP and every later call returns ASRKF_ESTATE until destroy.
  *    asrkf_last_error() gives a message for the calling thread.

@@ -37,7 +37,8 @@ design notes with the evidence for it):
   layers, relevance averaged over layers) instead of per-(layer, sequence)
   states; freeze candidates taken inside the window of the K most recent
   positions (the wording of Sec. 3.2) instead of outside it;
-* recovery (parity unpinned: the paper proposes but never evaluates it):
+* recovery (the paper proposes but never evaluates it, so no printed value
+  pins it; hand-derived expected states under these readings do):
   a step whose entropy exceeds theta_H (or whose top probability falls below
   theta_p when theta_p > 0) raises the sequence's escalation count by one, a
   calm step resets it; level = min(count, 3) selects SR, WR or FR, a count of

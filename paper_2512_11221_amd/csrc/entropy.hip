@@ -8,7 +8,9 @@
 // triples, one per lane, merges them in a fixed lane tree and forms
 //     H = ln S - T / S          (nats, softmax at temperature 1)
 //     p_max = 1 / S,
-// then updates the sequence's escalation count (one level per consecutive
+// A logit of -inf has probability 0 and adds nothing; a row with no finite
+// logit has no distribution: its entropy is NaN and it triggers nothing.
+// Then the kernel updates the sequence's escalation count (one level per consecutive
 // spike step, reset by a calm step) and writes the level that the end-of-step
 // compaction applies: 1 SR, 2 WR, 3 FR; a count above 3 also records a
 // Rewalk Regeneration request.
@@ -45,13 +47,16 @@ __device__ __forceinline__ Triple triple_of(const float (&x)[N], const bool (&ok
     float m = -INFINITY;
 #pragma unroll
     for (int i = 0; i < N; ++i) m = ok[i] ? fmaxf(m, x[i]) : m;
+    // no finite logit: an empty triple (a -inf logit has probability 0)
+    if (m == -INFINITY) return Triple{-INFINITY, 0.f, 0.f};
     float S = 0.f, T = 0.f;
 #pragma unroll
     for (int i = 0; i < N; ++i) {
         const float d = x[i] - m;
         const float e = ok[i] ? __builtin_amdgcn_exp2f(d * kLog2e) : 0.f;
         S += e;
-        T = fmaf(e, ok[i] ? d : 0.f, T);
+        // a term with e = 0 adds nothing (0 ln 0 = 0), also where d = -inf
+        T = fmaf(e, (ok[i] && e > 0.f) ? d : 0.f, T);
     }
     return Triple{m, S, T};
 }

@@ -152,7 +152,9 @@ struct asrkf_ctx {
     bool lists_ready = false;
     bool poisoned = false;
     bool timing = false;
-    hipStream_t last_stream = nullptr;
+    hipStream_t last_stream = nullptr;  // stream of the last call that queued work
+    bool queued = false;                // some call has queued work on last_stream
+    hipEvent_t ev_switch = nullptr;     // orders a call on a new stream after last_stream
     std::vector<std::pair<hipEvent_t, hipEvent_t>> ev_used, ev_free;
     double attn_ms_done = 0.0;
     int64_t attn_launches = 0;
@@ -216,6 +218,7 @@ void free_all(asrkf_ctx* ctx) {
     if (ctx->side) (void)hipStreamDestroy(ctx->side);
     if (ctx->ev_lists) (void)hipEventDestroy(ctx->ev_lists);
     if (ctx->ev_flag) (void)hipEventDestroy(ctx->ev_flag);
+    if (ctx->ev_switch) (void)hipEventDestroy(ctx->ev_switch);
     for (hipEvent_t e : ctx->ev_in) if (e) (void)hipEventDestroy(e);
     for (auto& ev : ctx->ev_used) { (void)hipEventDestroy(ev.first); (void)hipEventDestroy(ev.second); }
     for (auto& ev : ctx->ev_free) { (void)hipEventDestroy(ev.first); (void)hipEventDestroy(ev.second); }
@@ -271,6 +274,21 @@ asrkf_status validate(const asrkf_config* c) {
 }
 
 bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15) == 0; }
+
+// The context's arrays (cache, token states, lists, split partials) are shared
+// by every call, so a call on another stream than the previous one first waits
+// for everything that call queued.
+hipError_t follow_last_stream(asrkf_ctx* ctx, hipStream_t s) {
+    if (!ctx->queued || s == ctx->last_stream) return hipSuccess;
+    hipError_t e = hipEventRecord(ctx->ev_switch, ctx->last_stream);
+    if (e == hipSuccess) e = hipStreamWaitEvent(s, ctx->ev_switch, 0);
+    return e;
+}
+
+void mark_queued(asrkf_ctx* ctx, hipStream_t s) {
+    ctx->last_stream = s;
+    ctx->queued = true;
+}
 
 }  // namespace
 
@@ -410,6 +428,16 @@ asrkf_status asrkf_init(const asrkf_config* cfg, asrkf_ctx** out) {
     }
 #undef ALLOC
 
+    {
+        const hipError_t he = hipEventCreateWithFlags(&ctx->ev_switch, hipEventDisableTiming);
+        if (he != hipSuccess) {
+            st = hip_fail(nullptr, he, "hipEventCreateWithFlags");
+            free_all(ctx);
+            delete ctx;
+            return st;
+        }
+    }
+
     std::vector<int32_t> table(ctx->dur_len);
     for (int i = 0; i < ctx->dur_len; ++i) table[i] = exact_duration((uint64_t)i, c.k_soft);
 #define INIT(expr)                                                              \
@@ -456,6 +484,7 @@ asrkf_status asrkf_prefill(asrkf_ctx* ctx, int32_t layer, int32_t seq, const voi
         return fail(ASRKF_EINVAL, "sequence %d was prefilled with %d tokens in another layer",
                     seq, ctx->plen_host[seq]);
     hipStream_t s = static_cast<hipStream_t>(stream);
+    HIP_OK(ctx, follow_last_stream(ctx, s));
     const size_t off = ((size_t)layer * c.batch + seq) * ctx->pool_rows * ctx->row_bytes;
     const size_t bytes = (size_t)n_tokens * ctx->row_bytes;
     HIP_OK(ctx, hipMemcpyAsync((char*)ctx->kpool + off, k, bytes, hipMemcpyDeviceToDevice, s));
@@ -466,7 +495,7 @@ asrkf_status asrkf_prefill(asrkf_ctx* ctx, int32_t layer, int32_t seq, const voi
         HIP_OK(ctx, hipMemcpyAsync(ctx->plen + seq, &ctx->plen_host[seq], 4,
                                    hipMemcpyHostToDevice, s));
     }
-    ctx->last_stream = s;
+    mark_queued(ctx, s);
     return ASRKF_OK;
 }
 
@@ -610,6 +639,8 @@ asrkf_status asrkf_decode_step(asrkf_ctx* ctx, int32_t layer, const void* q, con
     st = check_overflow(ctx, false);
     if (st != ASRKF_OK) return st;
     hipStream_t s = static_cast<hipStream_t>(stream);
+    HIP_OK(ctx, follow_last_stream(ctx, s));
+    mark_queued(ctx, s);
     if (!ctx->lists_ready) {
         if (ctx->spill)
             for (int b = 0; b < c.batch; ++b)
@@ -719,7 +750,6 @@ asrkf_status asrkf_decode_step(asrkf_ctx* ctx, int32_t layer, const void* q, con
     }
 
     ctx->next_layer = layer + 1;
-    ctx->last_stream = s;
     return ASRKF_OK;
 }
 
@@ -735,6 +765,8 @@ asrkf_status asrkf_restore(asrkf_ctx* ctx, const float* logits, int32_t mode, vo
     st = check_overflow(ctx, false);
     if (st != ASRKF_OK) return st;
     hipStream_t s = static_cast<hipStream_t>(stream);
+    HIP_OK(ctx, follow_last_stream(ctx, s));
+    mark_queued(ctx, s);
     int forced;
     if (logits) {
         EntropyArgs e{};
@@ -761,16 +793,17 @@ asrkf_status asrkf_restore(asrkf_ctx* ctx, const float* logits, int32_t mode, vo
     }
     ctx->t += 1;
     ctx->next_layer = 0;
-    st = build_lists(ctx, forced, s);
-    ctx->last_stream = s;
-    return st;
+    return build_lists(ctx, forced, s);
 }
 
 namespace {
 
+// Everything the context queued: its calls are ordered on last_stream (a call
+// on a new stream waits for the previous one), except the spill-mode copies
+// on the side stream, which the next decode_step waits for.
 asrkf_status sync_ctx(asrkf_ctx* ctx) {
     HIP_OK(ctx, hipStreamSynchronize(ctx->last_stream));
-    HIP_OK(ctx, hipDeviceSynchronize());
+    if (ctx->side) HIP_OK(ctx, hipStreamSynchronize(ctx->side));
     return ASRKF_OK;
 }
 
@@ -950,7 +983,8 @@ asrkf_status asrkf_get_seq(asrkf_ctx* ctx, int32_t seq, float* entropy, float* p
 
 void asrkf_destroy(asrkf_ctx* ctx) {
     if (!ctx) return;
-    (void)hipDeviceSynchronize();
+    (void)hipStreamSynchronize(ctx->last_stream);
+    if (ctx->side) (void)hipStreamSynchronize(ctx->side);
     free_all(ctx);
     delete ctx;
 }

@@ -218,11 +218,20 @@ def _dev(x, dtype):
 
 
 def run_gpu(w, inp, instances, modes=None, with_logits=True, steps=None, record=None,
-            timing=False, side_delay_us=0):
+            timing=False, side_delay_us=0, streams=None):
     """Run the library; per instance a list of dict(out, unfreeze, count, frozen,
-    active_next) for the recorded steps; per sequence the entropy monitor."""
+    active_next) for the recorded steps; per sequence the entropy monitor.
+    streams(call, t, layer), when given, names the torch stream of each call
+    ("prefill", "decode", "restore"; None = the current stream); such a stream
+    first waits for the current stream, where the inputs were copied."""
     import torch
     import paper_2512_11221_amd as A
+
+    def on(call, t, layer):
+        s = streams(call, t, layer) if streams else None
+        if s is not None:
+            s.wait_stream(torch.cuda.current_stream())
+        return s
 
     steps = w.steps if steps is None else steps
     cfg = A.make_config(w.n_layers, w.batch, w.n_q_heads, w.n_kv_heads, w.head_dim,
@@ -242,7 +251,9 @@ def run_gpu(w, inp, instances, modes=None, with_logits=True, steps=None, record=
             for b in range(w.batch):
                 K, V = inp.prompt(l, b)
                 if len(K):
-                    A.asrkf_prefill(ctx, l, b, _dev(K, w.dtype), _dev(V, w.dtype), len(K))
+                    dk, dv = _dev(K, w.dtype), _dev(V, w.dtype)
+                    A.asrkf_prefill(ctx, l, b, dk, dv, len(K), stream=on("prefill", 0, l))
+                    torch.cuda.synchronize()
         torch.cuda.synchronize()
         for t in range(1, steps + 1):
             outs = []
@@ -254,16 +265,16 @@ def run_gpu(w, inp, instances, modes=None, with_logits=True, steps=None, record=
                 dq, dk, dv = _dev(q, w.dtype), _dev(kn, w.dtype), _dev(vn, w.dtype)
                 out = torch.empty((w.batch, w.n_q_heads, w.head_dim), dtype=torch.float32,
                                   device="cuda")
-                A.asrkf_decode_step(ctx, l, dq, dk, dv, out)
+                A.asrkf_decode_step(ctx, l, dq, dk, dv, out, stream=on("decode", t, l))
                 keep += [dq, dk, dv]
                 outs.append(out)
             mode = A.AUTO if modes is None else modes.get(t, A.NONE)
             if with_logits:
                 lg = _dev(np.stack([inp.logits(b, t) for b in range(w.batch)]), "f32")
                 keep.append(lg)
-                A.asrkf_restore(ctx, lg, mode)
+                A.asrkf_restore(ctx, lg, mode, stream=on("restore", t, None))
             else:
-                A.asrkf_restore(ctx, None, mode)
+                A.asrkf_restore(ctx, None, mode, stream=on("restore", t, None))
             torch.cuda.synchronize()
             if record is None or record(t):
                 for (l, b) in instances:
@@ -340,11 +351,12 @@ def compare_residency(w, gpu_recs, ora_recs):
     return restores
 
 
-def run_gpu_device(w, instances, record_steps, seqs_for_entropy=None):
+def run_gpu_device(w, instances, record_steps, seqs_for_entropy=None, check_state=None):
     """Run a large workload exactly as the bench does (device-generated inputs,
     the library's own launch configuration).  Returns per instance the attention
     output of every step and the token states at ``record_steps``; per sequence
-    the entropy monitor of every step."""
+    the entropy monitor of every step.  check_state(layer, seq, t, state), when
+    given, sees the token states of every (layer, sequence) at ``record_steps``."""
     import torch
     import paper_2512_11221_amd as A
     from synth.device import DeviceGen
@@ -390,6 +402,11 @@ def run_gpu_device(w, instances, record_steps, seqs_for_entropy=None):
                     st = A.asrkf_get_state(ctx, l, b, w.max_ctx)
                     st["t"] = t
                     states[(l, b)][t] = st
+            if check_state is not None and t in record_steps:
+                for l in range(L):
+                    for b in range(B):
+                        st = A.asrkf_get_state(ctx, l, b, w.max_ctx)
+                        check_state(l, b, t, st)
             for b in ent:
                 ent[b].append(A.asrkf_get_seq(ctx, b))
     finally:

@@ -20,7 +20,6 @@ What is checked, at a size the oracle cannot step through 2000 times:
   * from t_s - 1 on, the oracle stepped from that state: states and outputs
     at every step, the entropy level, the residency of every position.
 """
-import math
 
 import numpy as np
 import pytest
@@ -28,6 +27,7 @@ import pytest
 import oracle
 from synth import gen
 from tests import _harness as H
+from tests._closed_form import ClosedForm, base_trajectory
 
 pytestmark = pytest.mark.gpu
 
@@ -43,47 +43,6 @@ def gpu():
     import paper_2512_11221_amd as A
     A.load()
     return torch
-
-
-def _base_trajectory(k_soft, T):
-    """(count, frozen, remaining timer) after each of T steps of a token that is
-    a freeze candidate from step 1 and flagged whenever it attends: position 0
-    of an oracle instance with tau = +inf and no window (1 x 1 rows)."""
-    z = np.zeros((1, 1, 1))
-    inst = oracle.Instance(z, z, 0, math.inf, k_soft, capacity=T + 2)
-    c = np.zeros(T + 1, np.int64)
-    f = np.zeros(T + 1, bool)
-    r = np.zeros(T + 1, np.int64)
-    q = np.zeros((1, 1))
-    for t in range(1, T + 1):
-        inst.step(q, q, q)
-        timer, count, frozen = inst.state()
-        c[t], f[t], r[t] = count[0], frozen[0], timer[0]
-    return c, f, r
-
-
-class ClosedForm:
-    """Token states implied by the heavy-hitter recipe without recovery."""
-
-    def __init__(self, w, hot, base):
-        self.w, self.hot = w, hot
-        self.c, self.f, self.r = base
-        self.P, self.K = w.prefill[0], w.window_K
-
-    def state(self, t):
-        """(count, frozen, remaining timer) of positions 0..n_t-1 after step t."""
-        n = self.P + t
-        p = np.arange(n)
-        t0 = np.maximum(1, p - self.P + self.K + 1)          # first step outside the window
-        tau = np.where(self.hot[:n], 0, np.maximum(0, t - t0 + 1))
-        return self.c[tau], self.f[tau], np.where(self.f[tau], self.r[tau], 0)
-
-    def active(self, t):
-        """Positions attended at step t (after step t - 1), the new token last."""
-        if t == 1:
-            return np.arange(self.P + 1)
-        _, fz, _ = self.state(t - 1)
-        return np.concatenate([np.nonzero(~fz)[0], [self.P + t - 1]])
 
 
 def _oracle_out(q, K, V, A):
@@ -122,7 +81,7 @@ def test_recovery_stress_ctx131k():
     s_cold, s_hot = gen.hh_relevance_bounds(w0)
     assert s_cold < w0.tau - H.MARGIN and s_hot > w0.tau + H.MARGIN
 
-    base = _base_trajectory(w0.k_soft, SWITCH_AFTER + 200)
+    base = base_trajectory(w0.k_soft, SWITCH_AFTER + 200)
     c_b, f_b, r_b = base
     p_star = gen.plant_position(w0)
     # first step >= 2001 after which the planted token is frozen with remaining > 1

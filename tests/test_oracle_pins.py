@@ -246,8 +246,14 @@ def test_entropy_single_dominant_logit_is_zero():
 
 
 # --------------------------------------------------------------------------
-# Recovery ladder (reading of Sec. 3.6; the paper gives no numbers: unpinned)
+# Recovery ladder (Sec. 3.6).  The paper prints no numbers for it; the pins are
+# hand-derived expected states (tests/golden/recovery_levels.json) under the
+# readings of SR, WR, FR and the trigger stated there.
 # --------------------------------------------------------------------------
+
+RECOVERY = _golden("recovery_levels.json")
+_LEVEL = {"none": 0, "SR": O.SR, "WR": O.WR, "FR": O.FR}
+
 
 def test_escalation_ladder_sequence():
     spikes = {3, 5, 6, 9, 10, 11, 12, 13}
@@ -257,22 +263,55 @@ def test_escalation_ladder_sequence():
     assert [t for t, r in enumerate(rr) if r] == [12, 13]
 
 
-def test_recovery_levels_on_an_instance():
-    inst = _flag_all(40, 120, 8)
-    n = inst.n
-    F0 = set(np.nonzero(inst.frozen[:n])[0])
-    assert F0
-    timers = inst.timer[:n].copy()
-    a = _copy_instance(inst)
-    a.recover(O.SR, 16)
-    assert set(np.nonzero(a.frozen[:n])[0]) == {j for j in F0 if timers[j] <= 1}
-    b = _copy_instance(inst)
-    b.recover(O.WR, 16)
-    assert set(np.nonzero(b.frozen[:n])[0]) == {j for j in F0 if j < n - 16}
-    c = _copy_instance(inst)
-    c.recover(O.FR, 16)
-    assert not c.frozen[:n].any()
-    np.testing.assert_array_equal(c.count, inst.count)      # counts are kept
+@pytest.mark.parametrize("case", RECOVERY["escalation"]["cases"],
+                         ids=lambda c: f"thH{c['theta_H']}-thp{c['theta_p']}")
+def test_escalation_with_confidence_drop(case):
+    steps = [tuple(x) for x in RECOVERY["escalation"]["steps"]]
+    levels, rr = oracle.recovery_schedule(steps, float(case["theta_H"]), case["theta_p"])
+    assert levels == case["levels"]
+    assert [t for t, r in enumerate(rr) if r] == case["rr_steps"]
+
+
+def _static_state(cls=O.TokenStates):
+    g = RECOVERY["static_state"]
+    n = g["n"]
+    inst = cls(n + 1, 0, 0.0, 2.0)
+    inst.n = n
+    for j, rem in g["frozen_remaining"]:
+        inst.frozen[j] = True
+        inst.timer[j] = rem
+    inst.count[:n] = g["counts"]
+    return inst
+
+
+@pytest.mark.parametrize("level", ["SR", "WR", "FR"])
+def test_recovery_levels_static_state(level):
+    g = RECOVERY["static_state"]
+    inst = _static_state()
+    inst.recover(_LEVEL[level], g["wr_last_N"])
+    assert np.nonzero(inst.frozen[: g["n"]])[0].tolist() == g["frozen_after"][level]
+    assert inst.count[: g["n"]].tolist() == g["counts"]        # detection counts are kept
+
+
+def _recovery_case(case, inst_cls=O.Instance):
+    g = RECOVERY["single_token"]
+    lo, hi = g["window"]
+    attends = []
+
+    def hook(t, rec, inst):
+        if lo <= t <= hi and 0 in rec.active:
+            attends.append(t)
+        if t == case["after_step"] and case["level"] != "none":
+            inst.recover(_LEVEL[case["level"]], case["wr_last_N"])
+
+    _flag_all(g["prompt"], hi, g["window_K"], g["k"], hook, inst_cls=inst_cls)
+    return attends
+
+
+@pytest.mark.parametrize("case", RECOVERY["single_token"]["cases"],
+                         ids=lambda c: f"{c['level']}-after{c['after_step']}-N{c['wr_last_N']}")
+def test_recovery_on_the_single_token_trajectory(case):
+    assert _recovery_case(case) == case["attends"]
 
 
 def _copy_instance(inst):
@@ -341,3 +380,75 @@ def test_planted_attention_scale_mistake_breaks_sdpa(monkeypatch):
     monkeypatch.setattr(oracle, "attention", unscaled)
     with pytest.raises(AssertionError):
         test_attention_matches_torch_sdpa()
+
+
+# Planted mistakes in the recovery ladder: each must break a hand-derived pin.
+
+class _SoftResetAtOne(O.Instance):
+    """SR also restores tokens with one step to go."""
+    def recover(self, level, last_N):
+        if level == O.SR:
+            F = np.nonzero(self.frozen[: self.n])[0]
+            sel = F[self.timer[F] >= 1]
+            self.frozen[sel] = False
+            self.timer[sel] = 0
+        else:
+            super().recover(level, last_N)
+
+
+class _WindowResetOneWider(O.Instance):
+    """WR reaches one position further back (positions >= n - N - 1)."""
+    def recover(self, level, last_N):
+        super().recover(level, last_N + 1 if level == O.WR else last_N)
+
+
+class _WindowResetOneNarrower(O.Instance):
+    """WR stops one position short (positions >= n - N + 1)."""
+    def recover(self, level, last_N):
+        super().recover(level, last_N - 1 if level == O.WR else last_N)
+
+
+class _FullResetClearsCounts(O.Instance):
+    """FR also clears the detection counts."""
+    def recover(self, level, last_N):
+        super().recover(level, last_N)
+        if level == O.FR:
+            self.count[: self.n] = 0
+
+
+@pytest.mark.parametrize("cls", [_SoftResetAtOne, _WindowResetOneWider, _WindowResetOneNarrower,
+                                 _FullResetClearsCounts])
+def test_planted_recovery_mistakes_break_the_trajectories(cls):
+    cases = RECOVERY["single_token"]["cases"]
+    assert any(_recovery_case(c, cls) != c["attends"] for c in cases)
+
+
+def _trigger_ignores_theta_p(count, H, pmax, theta_H, theta_p):
+    spike = H > theta_H
+    count = count + 1 if spike else 0
+    return count, min(count, O.FR), count > O.FR
+
+
+def _trigger_non_strict_drop(count, H, pmax, theta_H, theta_p):
+    spike = (H > theta_H) or (theta_p > 0 and pmax <= theta_p)
+    count = count + 1 if spike else 0
+    return count, min(count, O.FR), count > O.FR
+
+
+def _trigger_rr_at_level_three(count, H, pmax, theta_H, theta_p):
+    spike = (H > theta_H) or (theta_p > 0 and pmax < theta_p)
+    count = count + 1 if spike else 0
+    return count, min(count, O.FR), count >= O.FR
+
+
+@pytest.mark.parametrize("variant", [_trigger_ignores_theta_p, _trigger_non_strict_drop,
+                                     _trigger_rr_at_level_three])
+def test_planted_trigger_mistakes_break_the_escalation_pin(monkeypatch, variant):
+    monkeypatch.setattr(O, "escalate", variant)
+    broken = False
+    for case in RECOVERY["escalation"]["cases"]:
+        try:
+            test_escalation_with_confidence_drop(case)
+        except AssertionError:
+            broken = True
+    assert broken
