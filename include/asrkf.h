@@ -169,6 +169,25 @@ asrkf_status asrkf_decode_step(asrkf_ctx* ctx, int32_t layer, const void* q,
                                const void* k_new, const void* v_new, float* out,
                                void* stream);
 
+/* asrkf_decode_step for callers that cannot allocate device memory when they
+ * call (code under HIP graph capture, serving loops, harnesses that forbid
+ * hipMalloc).  Same arguments, work and results as asrkf_decode_step (the same
+ * kernels); it allocates nothing and creates no event.  Its split-K partials
+ * (per partial slot and query head: head_dim + 2 floats; slots = attention
+ * grid + batch, where the grid is the number of attention workgroups resident
+ * at once, one per compute unit at the LLaMA-3-8B shape) live in a static
+ * device array of 32 MiB that the library holds on every GPU it runs on until
+ * the process ends; asrkf_init resolves its address on the context's device.
+ * EINVAL, with nothing done, when the partials of this context exceed 32 MiB
+ * ((grid + batch) * n_q_heads * (head_dim + 2) * 4 + 8 * batch bytes).  Every
+ * call on one GPU shares the array and leaves its contents behind: calls on
+ * one context are ordered (as for every call), but calls of different
+ * contexts that overlap on one GPU (unordered streams) race.  Attention
+ * timing (asrkf_set_timing) is not recorded by this call.  Asynchronous. */
+asrkf_status asrkf_decode_step_static(asrkf_ctx* ctx, int32_t layer, const void* q,
+                                      const void* k_new, const void* v_new, float* out,
+                                      void* stream);
+
 /* End the step: entropy of each sequence's next-token distribution and the
  * recovery ladder (Sec. 3.6), then the timer loop and the active caches of
  * the next step (Algorithm 1 timer loop; Sec. 3.5).

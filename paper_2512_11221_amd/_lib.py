@@ -77,6 +77,7 @@ def load():
         "asrkf_init": ([ctypes.POINTER(asrkf_config), ctypes.POINTER(P)], I32),
         "asrkf_prefill": ([P, I32, I32, P, P, I32, P], I32),
         "asrkf_decode_step": ([P, I32, P, P, P, P, P], I32),
+        "asrkf_decode_step_static": ([P, I32, P, P, P, P, P], I32),
         "asrkf_restore": ([P, P, I32, P], I32),
         "asrkf_stats": ([P, ctypes.POINTER(asrkf_stats_t)], I32),
         "asrkf_stats_reset": ([P], I32),
@@ -160,6 +161,11 @@ def asrkf_prefill(ctx, layer, seq, k, v, n_tokens, stream=None):
 def asrkf_decode_step(ctx, layer, q, k_new, v_new, out, stream=None):
     _check(load().asrkf_decode_step(ctx, layer, _ptr(q), _ptr(k_new), _ptr(v_new), _ptr(out),
                                     _stream(stream)))
+
+
+def asrkf_decode_step_static(ctx, layer, q, k_new, v_new, out, stream=None):
+    _check(load().asrkf_decode_step_static(ctx, layer, _ptr(q), _ptr(k_new), _ptr(v_new),
+                                           _ptr(out), _stream(stream)))
 
 
 def asrkf_restore(ctx, logits, mode=AUTO, stream=None):

@@ -20,6 +20,7 @@
 #include <string.h>
 
 #include <algorithm>
+#include <mutex>
 #include <string>
 #include <utility>
 #include <vector>
@@ -73,6 +74,16 @@ int32_t exact_duration(uint64_t c, float k) {
 }
 
 bool valid_k(float k) { return isfinite(k) && k >= 0x1p-8f && k <= 0x1p16f; }
+
+// Split-K partials of asrkf_decode_step_static: a fixed device array, so that
+// the call allocates nothing.  Every GPU the library runs on holds its own
+// copy until the process ends.  Host code never uses the array's name as an
+// address: each device's address is looked up once (asrkf_init) and kept.
+constexpr size_t kStaticScratchBytes = (size_t)32 << 20;
+__device__ __align__(256) unsigned char scratch[kStaticScratchBytes];
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch[kMaxDevices] = {};
 
 }  // namespace
 
@@ -161,6 +172,7 @@ struct asrkf_ctx {
     int64_t host_recoveries[4] = {0, 0, 0, 0};
     int side_delay_us = 0;              // test hook: side stream waits before its copies
     int device = 0;
+    void* static_scratch = nullptr;     // this device's address of the static partials array
 };
 
 namespace {
@@ -325,6 +337,17 @@ asrkf_status asrkf_init(const asrkf_config* cfg, asrkf_ctx** out) {
     hipDeviceProp_t prop;
     e = hipGetDeviceProperties(&prop, ctx->device);
     if (e != hipSuccess) { delete ctx; return hip_fail(nullptr, e, "hipGetDeviceProperties"); }
+    if (ctx->device >= 0 && ctx->device < kMaxDevices) {
+        // the static partials' address on this device (it is current here), once per device
+        std::lock_guard<std::mutex> lock(g_scratch_mu);
+        if (!g_scratch[ctx->device]) {
+            void* p = nullptr;
+            e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+            if (e != hipSuccess) { delete ctx; return hip_fail(nullptr, e, "hipGetSymbolAddress(scratch)"); }
+            g_scratch[ctx->device] = p;
+        }
+        ctx->static_scratch = g_scratch[ctx->device];
+    }
     // persistent grid: as many attention workgroups as can be resident at once
     {
         AttnArgs probe{};
@@ -499,6 +522,8 @@ asrkf_status asrkf_prefill(asrkf_ctx* ctx, int32_t layer, int32_t seq, const voi
     return ASRKF_OK;
 }
 
+}  // extern "C"
+
 namespace {
 
 asrkf_status build_lists(asrkf_ctx* ctx, int forced_level, hipStream_t s) {
@@ -621,12 +646,29 @@ asrkf_status check_overflow(asrkf_ctx* ctx, bool synced) {
 
 }  // namespace
 
-asrkf_status asrkf_decode_step(asrkf_ctx* ctx, int32_t layer, const void* q, const void* k_new,
-                               const void* v_new, float* out, void* stream) {
-    TraceRange range("asrkf_decode_step");
+namespace {
+
+// Bytes of the split partials (acc, (m, l), slot range per sequence).
+size_t partial_bytes(const asrkf_ctx* ctx) {
+    const asrkf_config& c = ctx->cfg;
+    return (size_t)ctx->n_slots * c.n_q_heads * (c.head_dim + 2) * 4 + (size_t)c.batch * 2 * 4;
+}
+
+// decode_step with its split partials in the context's scratch, or (use_static)
+// in the static array, with no event of its own.
+asrkf_status decode_step_impl(asrkf_ctx* ctx, int32_t layer, const void* q, const void* k_new,
+                              const void* v_new, float* out, void* stream, bool use_static) {
     asrkf_status st = check_ctx(ctx);
     if (st != ASRKF_OK) return st;
     const asrkf_config& c = ctx->cfg;
+    if (use_static) {
+        if (!ctx->static_scratch)
+            return fail(ASRKF_EINVAL, "no static scratch on device %d (devices 0..%d only)",
+                        ctx->device, kMaxDevices - 1);
+        if (partial_bytes(ctx) > kStaticScratchBytes)
+            return fail(ASRKF_EINVAL, "split partials of %zu bytes exceed the static scratch of %zu "
+                        "bytes; use asrkf_decode_step", partial_bytes(ctx), kStaticScratchBytes);
+    }
     if (layer != ctx->next_layer)
         return fail(ASRKF_ESTATE, "decode_step expected layer %d, got %d", ctx->next_layer, layer);
     if (!q || !k_new || !v_new || !out) return fail(ASRKF_EINVAL, "null argument");
@@ -685,6 +727,13 @@ asrkf_status asrkf_decode_step(asrkf_ctx* ctx, int32_t layer, const void* q, con
     a.part_ml = ctx->part_ml;
     a.slot_first = ctx->slot_info;
     a.slot_end = ctx->slot_info + c.batch;
+    if (use_static) {
+        float* base = static_cast<float*>(ctx->static_scratch);
+        a.part_acc = base;
+        a.part_ml = base + (size_t)ctx->n_slots * c.n_q_heads * c.head_dim;
+        a.slot_first = reinterpret_cast<int32_t*>(a.part_ml + (size_t)ctx->n_slots * c.n_q_heads * 2);
+        a.slot_end = a.slot_first + c.batch;
+    }
     a.B = c.batch;
     a.cap = ctx->cap;
     a.Hq = c.n_q_heads;
@@ -697,7 +746,7 @@ asrkf_status asrkf_decode_step(asrkf_ctx* ctx, int32_t layer, const void* q, con
     a.scale_log2 = (float)(1.4426950408889634 / sqrt((double)c.head_dim));
 
     std::pair<hipEvent_t, hipEvent_t> ev{nullptr, nullptr};
-    if (ctx->timing) {
+    if (ctx->timing && !use_static) {
         if (!ctx->ev_free.empty()) {
             ev = ctx->ev_free.back();
             ctx->ev_free.pop_back();
@@ -710,11 +759,11 @@ asrkf_status asrkf_decode_step(asrkf_ctx* ctx, int32_t layer, const void* q, con
     }
     HIP_OK(ctx, launch_attention(a, c.dtype == ASRKF_BF16, c.head_dim, ctx->group, ctx->grid, s,
                                  ev.first, ev.second));
-    if (ctx->timing) ctx->ev_used.push_back(ev);
+    if (ev.first) ctx->ev_used.push_back(ev);
 
     FinishArgs f{};
-    f.part_acc = ctx->part_acc;
-    f.part_ml = ctx->part_ml;
+    f.part_acc = a.part_acc;
+    f.part_ml = a.part_ml;
     f.slot_first = a.slot_first;
     f.slot_end = a.slot_end;
     f.out = out;
@@ -751,6 +800,23 @@ asrkf_status asrkf_decode_step(asrkf_ctx* ctx, int32_t layer, const void* q, con
 
     ctx->next_layer = layer + 1;
     return ASRKF_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+asrkf_status asrkf_decode_step(asrkf_ctx* ctx, int32_t layer, const void* q, const void* k_new,
+                               const void* v_new, float* out, void* stream) {
+    TraceRange range("asrkf_decode_step");
+    return decode_step_impl(ctx, layer, q, k_new, v_new, out, stream, false);
+}
+
+asrkf_status asrkf_decode_step_static(asrkf_ctx* ctx, int32_t layer, const void* q,
+                                      const void* k_new, const void* v_new, float* out,
+                                      void* stream) {
+    TraceRange range("asrkf_decode_step_static");
+    return decode_step_impl(ctx, layer, q, k_new, v_new, out, stream, true);
 }
 
 asrkf_status asrkf_restore(asrkf_ctx* ctx, const float* logits, int32_t mode, void* stream) {
@@ -796,6 +862,8 @@ asrkf_status asrkf_restore(asrkf_ctx* ctx, const float* logits, int32_t mode, vo
     return build_lists(ctx, forced, s);
 }
 
+}  // extern "C"
+
 namespace {
 
 // Everything the context queued: its calls are ordered on last_stream (a call
@@ -820,6 +888,8 @@ asrkf_status collect_timing(asrkf_ctx* ctx) {
 }
 
 }  // namespace
+
+extern "C" {
 
 asrkf_status asrkf_stats(asrkf_ctx* ctx, asrkf_stats_t* out) {
     asrkf_status st = check_ctx(ctx);
