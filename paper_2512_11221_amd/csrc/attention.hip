@@ -1,11 +1,13 @@
-// Active-set GQA flash-decode for gfx950, fused with the relevance score and
-// the freeze schedule, and the per-layer split combine.
+// Active-set GQA flash-decode for gfx950, fused with the relevance score, and
+// the per-layer split combine.
 //
 // Per launch (one layer, every sequence):
 //   Eq. 1  o_h = softmax_j(q_h . k_j / sqrt(D)) v_j over the active list A_t;
-//   Eq. 2  s_j = (1/Hq) sum_h |q_h . k_j| for every j in A_t;
-//   Alg. 1 freeze loop: j outside the window with s_j < tau gets c_j += 1 and,
-//          when d = floor(sqrt(c_j)/k) >= 1, the unfreeze step U_j = t + d.
+//   Eq. 2  s_j = (1/Hq) sum_h |q_h . k_j| for every j in A_t, and the flag
+//          s_j < tau stored per position; Algorithm 1's freeze loop reads the
+//          flags at the end of the step (in the list rebuild, which streams
+//          every position's state anyway), so no count or unfreeze step is
+//          read or written here.
 //
 // Work decomposition.  The active lists of all sequences, concatenated (each
 // preceded by a few virtual tokens that stand for the fixed cost of a
@@ -26,8 +28,8 @@
 // instruction moves 8 contiguous 128-byte segments.  A slot's row serves the
 // G query heads of its KV head from registers (GQA sharing); dot products are
 // reduced over the slot's 8 lanes with DPP, the relevance over the token's
-// KV-head slots with lane exchanges, so the freeze decision is made in the
-// wave and applied by the workgroup after each chunk.
+// KV-head slots with lane exchanges, so the score flag is decided in the
+// wave and stored by the workgroup after each chunk.
 //
 // Wide groups and many KV heads.  With G = 8 a slot holds a virtual KV head,
 // one KV head with half of its query heads (two slots read the same row, in
@@ -40,7 +42,7 @@ namespace asrkf {
 namespace {
 
 constexpr int kWaves = 8;           // waves per workgroup
-constexpr int kChunk = 2048;        // tokens per LDS chunk (positions, freeze flags)
+constexpr int kChunk = 2048;        // tokens per LDS chunk (positions, score flags)
 constexpr int kMinPerGroup = 32;    // fewest tokens worth a workgroup
 // Each sequence a workgroup takes part in costs it a fixed set-up and merge
 // (list staging, q, the freeze loop, the wave-state merge, a partial), about
@@ -48,7 +50,6 @@ constexpr int kMinPerGroup = 32;    // fewest tokens worth a workgroup
 // tokens ahead of every non-empty list, so a workgroup whose range straddles
 // two sequences gets correspondingly fewer real tokens.
 constexpr int kSeqCost = 48;
-constexpr int kDurCache = 512;      // Eq. 3 durations cached in LDS
 constexpr int kStage = kChunk / (64 * kWaves);   // chunk entries per thread
 // raw buffer descriptor word 3 for gfx9-class targets (32-bit data, no swizzle)
 constexpr int kBufferFlags = 0x00020000;
@@ -270,8 +271,7 @@ attention_kernel(AttnArgs a) {
     extern __shared__ int32_t lds[];
     __shared__ unsigned tile_lead;                               // most tiles any wave has finished
     int32_t* seq_off = lds;                                      // [B + 1]
-    int32_t* dur_lds = lds + ((a.B + 1 + 3) & ~3);               // [kDurCache]
-    int32_t* pos_lds = dur_lds + kDurCache;                      // [kChunk]
+    int32_t* pos_lds = lds + ((a.B + 1 + 3) & ~3);               // [kChunk]
     int32_t* row_lds = pos_lds + kChunk;                         // [kChunk] (spill mode)
     float* rel_lds = reinterpret_cast<float*>(row_lds + kChunk);   // [kChunk][NWG <= 4] (token
                                                                  // scope; the parts' sums)
@@ -279,11 +279,7 @@ attention_kernel(AttnArgs a) {
     // the wave-state merge runs after the chunk loop: it reuses the chunk buffers
     float* merge_lds = reinterpret_cast<float*>(pos_lds);        // [kWaves/2][NV][64]
 
-    // the duration table's load overlaps the planner's (one memory round trip for both)
-    static_assert(kDurCache == 64 * kWaves, "one duration per thread");
-    const int dur_mine = a.dur[min((int)threadIdx.x, a.dur_len - 1)];
     plan_ranges(a.n_active, a.B, seq_off);
-    dur_lds[threadIdx.x] = dur_mine;
     __syncthreads();
     const int T = wave_uniform(seq_off[a.B]);
     const int Gn = active_groups(T, gridDim.x);
@@ -360,16 +356,14 @@ attention_kernel(AttnArgs a) {
             const int app_off = threadIdx.x * 16;
             const bool append = c0 + len == nb && app_off < row_stride;
             uint4 knew_piece, vnew_piece;
-            int spill_row = 0;
+            int new_row = 0;
             if (append) {
                 const size_t src = (size_t)b * row_stride + app_off;
                 knew_piece = *reinterpret_cast<const uint4*>((const char*)a.knew + src);
                 vnew_piece = *reinterpret_cast<const uint4*>((const char*)a.vnew + src);
-                if (spill) spill_row = lrow_b[nb - 1];
+                // the list's last entry is the new token (its position; its row in spill mode)
+                new_row = spill ? lrow_b[nb - 1] : list_b[nb - 1];
             }
-            const int n_pos = a.plen[b] + a.t;       // positions after the append
-            const int wedge = n_pos - a.window_K;    // positions < wedge are outside the window
-            const bool inside = a.cand_inside != 0;
             // stage the chunk's positions (and device rows): every load first, then the
             // stores; the query rows are requested in between, so the chunk's set-up
             // costs one memory round trip
@@ -405,7 +399,6 @@ attention_kernel(AttnArgs a) {
                 }
             }
             if (append) {
-                const int new_row = spill ? spill_row : n_pos - 1;
                 const size_t dst = seg + (size_t)new_row * row_stride + app_off;
                 *reinterpret_cast<uint4*>((char*)a.kpool_w + dst) = knew_piece;
                 *reinterpret_cast<uint4*>((char*)a.vpool_w + dst) = vnew_piece;
@@ -469,7 +462,7 @@ attention_kernel(AttnArgs a) {
                                 rel_lds[(tb + u * TPI + tk) * NWG + wpart] = rel;
                             } else if (scope_token) {
                                 rel_lds[tb + u * TPI + tk] = rel;
-                            } else if (rel < a.tau_H) {   // candidates are sorted out below
+                            } else if (rel < a.tau_H) {   // the freeze loop picks the candidates
                                 flag_lds[tb + u * TPI + tk] = 1;
                             }
                         }
@@ -559,39 +552,13 @@ attention_kernel(AttnArgs a) {
                     if (i < len) a.rel_acc[seq_row + pos_lds[i]] = prev[k] + rel_lds[i * NWG];
                 }
             }
-            // freeze loop over the chunk's flagged candidates (Alg. 1; Eq. 3); a flag
-            // says only that the score is below tau, the window test is made here,
-            // outside the tile loop
-            if (a.history_W == 0) {
-                // cumulative count: every count load first, then the updates
-                // (an entry without a flag reads the sequence's first count and ignores it)
-                int p[kStage], cnt[kStage];
-                bool f[kStage];
+            // score flags of the chunk's tokens (s_j < tau), one byte per position, for
+            // the freeze loop of the end-of-step rebuild (which tests the window)
+            if (rel_abs && !scope_token) {
 #pragma unroll
                 for (int k = 0; k < kStage; ++k) {
                     const int i = threadIdx.x + k * 64 * kWaves;
-                    const int pi = pos_lds[min(i, len - 1)];
-                    f[k] = i < len && flag_lds[i] && freeze_candidate(pi, wedge, inside);
-                    p[k] = f[k] ? pi : 0;
-                }
-#pragma unroll
-                for (int k = 0; k < kStage; ++k) cnt[k] = a.count[seq_row + p[k]];
-#pragma unroll
-                for (int k = 0; k < kStage; ++k) {
-                    if (!f[k]) continue;
-                    const size_t o = seq_row + p[k];
-                    const int c = cnt[k] + 1;
-                    a.count[o] = c;
-                    const int d = c < kDurCache ? dur_lds[c] : a.dur[min(c, a.dur_len - 1)];
-                    if (d >= 1) a.unfreeze[o] = a.t + d;
-                }
-            } else {
-                for (int i = threadIdx.x; i < len; i += blockDim.x) {
-                    if (!flag_lds[i] || !freeze_candidate(pos_lds[i], wedge, inside)) continue;
-                    const size_t o = seq_row + pos_lds[i];
-                    const int c = detect(a.count, a.hmask, a.hlast, o, a.t, a.history_W);
-                    const int d = c < kDurCache ? dur_lds[c] : a.dur[min(c, a.dur_len - 1)];
-                    if (d >= 1) a.unfreeze[o] = a.t + d;
+                    if (i < len) a.flag[seq_row + pos_lds[i]] = flag_lds[i];
                 }
             }
             __syncthreads();                       // LDS chunk buffers are reused next
@@ -847,7 +814,7 @@ size_t lds_bytes(const AttnArgs& a) {
     constexpr int GS = G / split_of<BF16, D, G>();
     const size_t merge = (size_t)(merge_one_round<BF16, D, GS>() ? kWaves : kWaves / 2) *
                          state_floats<BF16, D, GS>() * 64 * 4;
-    return (size_t)(((a.B + 1 + 3) & ~3) + kDurCache) * 4 + (chunk > merge ? chunk : merge);
+    return (size_t)((a.B + 1 + 3) & ~3) * 4 + (chunk > merge ? chunk : merge);
 }
 
 // Timing events, when given, are recorded by the dispatch itself, so they

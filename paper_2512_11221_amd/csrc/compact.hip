@@ -1,10 +1,14 @@
 // End-of-step rebuild of every active cache, with staged recovery fused in.
 //
 // One workgroup per (layer, sequence), or per sequence when the token states
-// are shared by all layers.  It streams the unfreeze steps U_p of the n_t
-// positions and:
-//   0. token scope only: runs the step's freeze loop (Algorithm 1) on the
-//      relevance summed over all layers, since no single layer can;
+// are shared by all layers.  It streams the unfreeze steps U_p, detection
+// counts c_p and score flags of the n_t positions and:
+//   0. runs the step's freeze loop (Algorithm 1): a position that attended
+//      step t (U_p <= t), is a freeze candidate and scored below tau gets
+//      c_p += 1 and, when d = floor(sqrt(c_p)/k) >= 1, U_p = t + d.  The
+//      verdict "below tau" is the flag byte the attention kernel wrote for
+//      the position at step t (layer scope), or in token scope the relevance
+//      summed over every layer, which no single layer's kernel can form;
 //   1. applies the recovery level chosen for the sequence (Sec. 3.6):
 //        SR: remaining timer U_p - (t+1) > 1     ->  U_p = t+1
 //        WR: p >= n_t - N and U_p > t+1          ->  U_p = t+1
@@ -46,6 +50,17 @@ __device__ __forceinline__ int lanes_below(unsigned long long mask) {
                                      __builtin_amdgcn_mbcnt_lo((unsigned)mask, 0));
 }
 
+__device__ __forceinline__ void load4(const int32_t* src, int p, int n, int (&v)[4], int fill) {
+    // p is a multiple of 4 and every array row starts 16-byte aligned
+    if (p + 3 < n) {
+        const int4 x = *reinterpret_cast<const int4*>(src + p);
+        v[0] = x.x; v[1] = x.y; v[2] = x.z; v[3] = x.w;
+    } else {
+#pragma unroll
+        for (int k = 0; k < 4; ++k) v[k] = (p + k < n) ? src[p + k] : fill;
+    }
+}
+
 struct Ladder {
     bool sr, wr, fr;
     int t1, wr_from;
@@ -56,22 +71,69 @@ __device__ __forceinline__ Ladder make_ladder(const CompactArgs& a, int b, int n
     return Ladder{level == 1, level == 2, level == 3, a.t + 1, n - a.wr_last_N};
 }
 
+// The freeze loop of step t over the 4 positions p .. p+3 of a thread (those
+// below hi): u, cnt are their U and c, flags their score flags (one byte
+// each, layer scope).  With a cumulative count (history_W = 0) the counts come
+// in with U and only changed entries are stored; a finite history window
+// updates the detection bits of a flagged position.  Returns whether u changed.
+__device__ __forceinline__ bool freeze4(const CompactArgs& a, size_t base, int p, int hi, int n,
+                                        int (&u)[4], const int (&cnt)[4], uint32_t flags) {
+    if (!a.freeze) return false;
+    bool dirty = false;
+    const bool inside = a.cand_inside != 0;
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+        const int q = p + k;
+        bool low;
+        if (a.scope_token) low = q < hi && a.rel_acc[base + q] < a.tau_LH;
+        else low = ((flags >> (8 * k)) & 0xFFu) != 0;
+        if (q < hi && u[k] <= a.t && low && freeze_candidate(q, n - a.window_K, inside)) {
+            int c;
+            if (a.history_W == 0) {
+                c = cnt[k] + 1;
+                a.count[base + q] = c;
+            } else {
+                c = detect(a.count, a.hmask, a.hlast, base + q, a.t, a.history_W);
+            }
+            const int d = a.dur[min(c, a.dur_len - 1)];
+            if (d >= 1) {
+                u[k] = a.t + d;
+                dirty = true;
+            }
+        }
+    }
+    return dirty;
+}
+
+// U, counts and flags of the 4 positions p .. p+3 (those below hi), as the
+// freeze loop reads them; counts and flags only when the step freezes.
+struct Tile4 {
+    int u[4], c[4];
+    uint32_t f;
+};
+
+__device__ __forceinline__ void load_tile(const CompactArgs& a, size_t base, int p, int hi, Tile4& x) {
+    load4(a.unfreeze + base, p, hi, x.u, 0);
+    x.f = 0;
+    if (a.freeze) {
+        if (a.history_W == 0) load4(a.count + base, p, hi, x.c, 0);
+        if (!a.scope_token) {
+            if (p + 3 < hi) {
+                x.f = *reinterpret_cast<const uint32_t*>(a.flag + base + p);
+            } else {
+#pragma unroll
+                for (int k = 0; k < 4; ++k) x.f |= (p + k < hi ? (uint32_t)a.flag[base + p + k] : 0u) << (8 * k);
+            }
+        }
+    }
+}
+
 // Recovery select of one position.  Written with bitwise operators only: one
 // select per position, no short-circuit control flow.
 __device__ __forceinline__ int recover(const Ladder& r, int u, int q, bool live, bool& hit) {
     const bool frozen_now = live & (u > r.t1);
     hit = frozen_now & ((r.sr & (u > r.t1 + 1)) | (r.wr & (q >= r.wr_from)) | r.fr);
     return hit ? r.t1 : u;
-}
-
-__device__ __forceinline__ void load4(const int32_t* src, int p, int n, int (&v)[4], int fill) {
-    if (p + 3 < n) {
-        const int4 x = *reinterpret_cast<const int4*>(src + p);
-        v[0] = x.x; v[1] = x.y; v[2] = x.z; v[3] = x.w;
-    } else {
-#pragma unroll
-        for (int k = 0; k < 4; ++k) v[k] = (p + k < n) ? src[p + k] : fill;
-    }
 }
 
 // Exclusive offsets inside the tile of up to two per-thread item counts, and
@@ -112,7 +174,7 @@ __device__ __forceinline__ void ballot4(const bool (&f)[4], int& before, int& mi
 }
 
 // The rebuild of positions [lo, hi) of one instance.  MODE 0 applies the
-// step's updates (token-scope freeze loop, recovery) and writes the list;
+// step's updates (freeze loop, recovery) and writes the list;
 // MODE 1 applies the updates and only counts; MODE 2 writes the list from
 // the already updated U.  List entries start at list + out_base.  Returns
 // the number of listed positions (the same value in every thread).
@@ -123,32 +185,20 @@ __device__ int compact_range(const CompactArgs& a, const Ladder& r, size_t base,
     int32_t* list = a.list + base;
     const int tid = threadIdx.x;
     int listed = 0;
-    int u_next[4];
-    load4(U, lo + 4 * tid, hi, u_next, 0);
+    Tile4 next;
+    if constexpr (MODE != 2) load_tile(a, base, lo + 4 * tid, hi, next);
+    else load4(U, lo + 4 * tid, hi, next.u, 0);
     for (int p0 = lo; p0 < hi; p0 += 4 * kThreads) {
         const int p = p0 + 4 * tid;
-        int u[4] = {u_next[0], u_next[1], u_next[2], u_next[3]};
-        if (p0 + 4 * kThreads < hi) load4(U, p + 4 * kThreads, hi, u_next, 0);   // next tile in flight
+        Tile4 cur = next;
+        int (&u)[4] = cur.u;
+        if (p0 + 4 * kThreads < hi) {                                            // next tile in flight
+            if constexpr (MODE != 2) load_tile(a, base, p + 4 * kThreads, hi, next);
+            else load4(U, p + 4 * kThreads, hi, next.u, 0);
+        }
         bool flag[4];
         if constexpr (MODE != 2) {
-            bool dirty = false;
-            if (a.scope_token) {
-                // token scope: Algorithm 1's freeze loop for the whole sequence, on the
-                // relevance summed over every layer's heads (state before this step: U <= t attended)
-#pragma unroll
-                for (int k = 0; k < 4; ++k) {
-                    const int q = p + k;
-                    if (q < hi && u[k] <= a.t && freeze_candidate(q, n - a.window_K, a.cand_inside != 0) &&
-                        a.rel_acc[base + q] < a.tau_LH) {
-                        const int c = detect(a.count, a.hmask, a.hlast, base + q, a.t, a.history_W);
-                        const int d = a.dur[min(c, a.dur_len - 1)];
-                        if (d >= 1) {
-                            u[k] = a.t + d;
-                            dirty = true;
-                        }
-                    }
-                }
-            }
+            bool dirty = freeze4(a, base, p, hi, n, u, cur.c, cur.f);
 #pragma unroll
             for (int k = 0; k < 4; ++k) {
                 bool hit;
@@ -262,15 +312,18 @@ compact_spill_kernel(CompactArgs a) {
     const int tid = threadIdx.x;
     const int top0 = a.free_top[inst];
 
-    // pass 1: recovery, then release the rows of tokens frozen now for d >= spill_min_D
+    // pass 1: the freeze loop and recovery, then release the rows of tokens
+    // frozen now for d >= spill_min_D
     int pushed = 0, n_out = 0;
     for (int p0 = 0; p0 < n; p0 += 4 * kThreads) {
         const int p = p0 + 4 * tid;
-        int u[4], row[4];
-        load4(U, p, n, u, 0);
+        Tile4 cur;
+        load_tile(a, base, p, n, cur);
+        int (&u)[4] = cur.u;
+        int row[4];
         load4(row_of, p, n, row, -1);
         bool spill[4], first[4];
-        bool dirty = false;
+        bool dirty = freeze4(a, base, p, n, n, u, cur.c, cur.f);
 #pragma unroll
         for (int k = 0; k < 4; ++k) {
             bool hit;
@@ -417,11 +470,13 @@ spill_count_kernel(CompactArgs a) {
     int ns = 0, nf = 0, nn = 0, nl = 0;
     for (int p0 = lo; p0 < hi; p0 += 4 * kThreads) {
         const int p = p0 + 4 * threadIdx.x;
-        int u[4], row[4];
-        load4(U, p, hi, u, 0);
+        Tile4 cur;
+        load_tile(a, base, p, hi, cur);
+        int (&u)[4] = cur.u;
+        int row[4];
         load4(row_of, p, hi, row, -1);
         bool spill[4], first[4], need[4], flag[4];
-        bool dirty = false;
+        bool dirty = freeze4(a, base, p, hi, n, u, cur.c, cur.f);
 #pragma unroll
         for (int k = 0; k < 4; ++k) {
             bool hit;

@@ -55,10 +55,9 @@ struct AttnArgs {
     const int32_t* list_row;  // layer base, [B][cap] device row of each listed position
                               // (spill mode only; in resident mode the row is the position)
     const int32_t* n_active;  // layer base, [B]
-    const int32_t* plen;      // [B] prompt length
-    int32_t* unfreeze;        // layer base, [B][cap]: U_j
-    int32_t* count;           // layer base, [B][cap]: c_j
-    const int32_t* dur;       // [dur_len] freeze duration by count (Eq. 3)
+    uint8_t* flag;            // layer base, [B][cap]: 1 where the attended position scores
+                              // below tau (Eq. 2), 0 where not; read by the freeze loop
+                              // at the end of the step
     float* part_acc;          // [grid + B][Hq][D]
     float* part_ml;           // [grid + B][Hq][2]: (max in log2 units, sum)
     int32_t* slot_first;      // [B] first partial slot of each sequence (written)
@@ -66,19 +65,12 @@ struct AttnArgs {
     int32_t B, cap, Hq, Hkv;
     int32_t pool_rows;        // device rows per sequence (cap in resident mode)
     int32_t spill;            // 1: rows come from list_row
-    int32_t t;                // current step (1-based)
-    int32_t window_K;
-    int32_t cand_inside;      // 1: freeze candidates inside the window, 0: outside
-    int32_t dur_len;
     float tau_H;              // tau * Hq: compared against sum_h |q_h . k_j|
     float scale_log2;         // log2(e) / sqrt(D)
     // relevance reading and state scope
     int32_t rel_mode;         // 0: Eq. 2 |q.k| scored here; 1: softmax weights (weight_relevance_kernel)
-    int32_t scope_token;      // 1: one token state per sequence; the freeze loop runs at the step's end
+    int32_t scope_token;      // 1: one token state per sequence, scored by the sum over layers
     int32_t first_layer;      // token scope: this launch starts the per-token sums
-    int32_t history_W;        // 0: cumulative detection count; else window in steps
-    uint64_t* hmask;          // state base [B][cap] (history window): detection bits, bit i = step hlast - i
-    int32_t* hlast;           // state base [B][cap]: step of the last detection
     float* rel_acc;           // token scope, [B][cap]: sum over layers and heads of the relevance
     float* xlog;              // softmax relevance, [B][cap][Hq]: q.k * log2(e)/sqrt(D) per listed token
 };
@@ -96,21 +88,15 @@ struct FinishArgs {
 
 // Relevance by attention weight, after the split combine of a layer:
 // s_j = sum_h 2^(y_hj - M_h) / L_h over the heads (compared with tau * Hq),
-// then the freeze loop (layer scope) or the per-token sum (token scope).
+// then the score flag (layer scope) or the per-token sum (token scope).
 struct RelevanceArgs {
     const float* xlog;        // [B][cap][Hq]
     const float* norm;        // [B][Hq][2]
     const int32_t* list;      // state base [B][cap]
     const int32_t* n_active;  // state base [B]
-    const int32_t* plen;
-    int32_t* unfreeze;        // state base [B][cap]
-    int32_t* count;
-    uint64_t* hmask;
-    int32_t* hlast;
-    const int32_t* dur;
+    uint8_t* flag;            // state base [B][cap]
     float* rel_acc;           // token scope [B][cap]
-    int32_t B, cap, Hq, t, window_K, dur_len, history_W, scope_token, first_layer;
-    int32_t cand_inside;      // 1: freeze candidates inside the window, 0: outside
+    int32_t B, cap, Hq, scope_token, first_layer;
     float tau_H;
 };
 
@@ -140,11 +126,13 @@ struct CompactArgs {
     int32_t* n_in;            // [L][B]
     int32_t* overflow;        // set to 1 when a sequence needs more device rows than it has
     unsigned long long* xfer; // [0] rows to host, [1] rows from host, [2] device rows released
-    // token scope: the freeze loop of the step runs here, before recovery
-    int32_t scope_token;
-    const float* rel_acc;     // [B][cap] relevance summed over layers and heads
+    // the freeze loop of step t runs here, before recovery (not before step 1)
+    int32_t freeze;           // 1: apply the step's freeze loop
+    const uint8_t* flag;      // [L][B][cap] layer scope: 1 where the position scored below tau at step t
+    int32_t scope_token;      // 1: one state per sequence, scored by the sum over layers
+    const float* rel_acc;     // [B][cap] token scope: relevance summed over layers and heads
     float tau_LH;             // tau * n_layers * Hq
-    int32_t* count;           // [B][cap]
+    int32_t* count;           // [L][B][cap] (or [B][cap] in token scope): c_j
     uint64_t* hmask;
     int32_t* hlast;
     const int32_t* dur;

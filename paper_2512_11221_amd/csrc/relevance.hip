@@ -4,10 +4,10 @@
 // which needs each head's normaliser over the whole active set.  The
 // attention kernel keeps y_hj = q_h . k_j * log2(e)/sqrt(d) of every listed
 // token, the split combine leaves (M_h, L_h) = (max, sum of 2^(y - M)), and
-// this kernel forms H * s_j = sum_h 2^(y_hj - M_h) / L_h.  It then runs the
-// freeze loop of Algorithm 1 for the layer (layer scope) or adds the score to
-// the token's sum over layers (token scope; the freeze loop runs at the end
-// of the step).  One thread per listed token.
+// this kernel forms H * s_j = sum_h 2^(y_hj - M_h) / L_h.  It then writes the
+// token's score flag (s_j < tau, layer scope) or adds the score to the
+// token's sum over layers (token scope); the freeze loop of Algorithm 1 runs
+// at the end of the step on either.  One thread per listed token.
 #include "kernels.h"
 
 namespace asrkf {
@@ -26,7 +26,6 @@ weight_relevance_kernel(RelevanceArgs a) {
     }
     __syncthreads();
     const int n = a.n_active[b];
-    const int wedge = a.plen[b] + a.t - a.window_K;     // positions < wedge are outside the window
     const size_t row = (size_t)b * a.cap;
     for (int i = blockIdx.x * kThreads + threadIdx.x; i < n; i += gridDim.x * kThreads) {
         const float* y = a.xlog + (row + i) * a.Hq;
@@ -34,13 +33,8 @@ weight_relevance_kernel(RelevanceArgs a) {
         for (int h = 0; h < a.Hq; ++h) s = fmaf(__builtin_amdgcn_exp2f(y[h] - M[h]), invL[h], s);
         const int pos = a.list[row + i];
         const size_t o = row + pos;
-        if (a.scope_token) {
-            a.rel_acc[o] = a.first_layer ? s : a.rel_acc[o] + s;
-        } else if (freeze_candidate(pos, wedge, a.cand_inside != 0) && s < a.tau_H) {
-            const int c = detect(a.count, a.hmask, a.hlast, o, a.t, a.history_W);
-            const int d = a.dur[min(c, a.dur_len - 1)];
-            if (d >= 1) a.unfreeze[o] = a.t + d;
-        }
+        if (a.scope_token) a.rel_acc[o] = a.first_layer ? s : a.rel_acc[o] + s;
+        else a.flag[o] = s < a.tau_H ? 1 : 0;
     }
 }
 

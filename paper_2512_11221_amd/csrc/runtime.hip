@@ -5,6 +5,7 @@
 //   K, V cache      [L][B][pool_rows][Hkv][D]   dtype   token-major rows
 //   unfreeze U      [L][B][cap]           int32   token attends at step t iff U <= t
 //   count c         [L][B][cap]           int32   low-relevance detections (Eq. 3)
+//   score flag      [L][B][cap]           uint8   s_j < tau at the current step (Eq. 2)
 //   active list     [L][B][cap]           int32   ascending positions for the step
 //   n_active        [L][B]                int32
 //   partials        [grid+B][Hq][D+2]     fp32    split-K attention partials
@@ -102,6 +103,7 @@ struct asrkf_ctx {
     void* vpool = nullptr;
     int32_t* unfreeze = nullptr;
     int32_t* count = nullptr;
+    uint8_t* flag = nullptr;
     int32_t* list = nullptr;
     int32_t* n_active = nullptr;
     int32_t* plen = nullptr;
@@ -217,7 +219,7 @@ asrkf_status dev_alloc(asrkf_ctx* ctx, T** p, size_t bytes) {
 }
 
 void free_all(asrkf_ctx* ctx) {
-    void* ptrs[] = {ctx->kpool, ctx->vpool, ctx->unfreeze, ctx->count, ctx->list,
+    void* ptrs[] = {ctx->kpool, ctx->vpool, ctx->unfreeze, ctx->count, ctx->flag, ctx->list,
                     ctx->n_active, ctx->plen, ctx->dur, ctx->escalation, ctx->level,
                     ctx->entropy, ctx->pmax, ctx->part_acc, ctx->part_ml, ctx->slot_info, ctx->ent_partial, ctx->ent_ticket,
                     ctx->counters, ctx->row_of, ctx->on_host, ctx->list_row, ctx->free_rows,
@@ -383,6 +385,7 @@ asrkf_status asrkf_init(const asrkf_config* cfg, asrkf_ctx** out) {
     ALLOC(vpool, pool_bytes);
     ALLOC(unfreeze, st_pos * 4);
     ALLOC(count, st_pos * 4);
+    ALLOC(flag, st_pos);
     ALLOC(list, st_pos * 4);
     if (c.history_W > 0) {
         ALLOC(hmask, st_pos * 8);
@@ -555,19 +558,20 @@ asrkf_status build_lists(asrkf_ctx* ctx, int forced_level, hipStream_t s) {
     a.n_seg = ctx->n_seg;
     a.seg_len = ctx->seg_len;
     a.seg_count = ctx->seg_count;
-    if (ctx->token_scope && ctx->t > 0) {    // the step's freeze loop (not before the first step)
-        a.scope_token = 1;
-        a.rel_acc = ctx->rel_acc;
-        a.tau_LH = ctx->cfg.tau * (float)ctx->cfg.n_layers * (float)ctx->cfg.n_q_heads;
-        a.count = ctx->count;
-        a.hmask = ctx->hmask;
-        a.hlast = ctx->hlast;
-        a.dur = ctx->dur;
-        a.dur_len = ctx->dur_len;
-        a.history_W = ctx->cfg.history_W;
-        a.window_K = ctx->cfg.window_K;
-        a.cand_inside = ctx->cfg.candidates == ASRKF_CAND_INSIDE;
-    }
+    // the freeze loop of the step that ends here (there is none before the first step)
+    a.freeze = ctx->t > 0 ? 1 : 0;
+    a.flag = ctx->flag;
+    a.scope_token = ctx->token_scope ? 1 : 0;
+    a.rel_acc = ctx->rel_acc;
+    a.tau_LH = ctx->cfg.tau * (float)ctx->cfg.n_layers * (float)ctx->cfg.n_q_heads;
+    a.count = ctx->count;
+    a.hmask = ctx->hmask;
+    a.hlast = ctx->hlast;
+    a.dur = ctx->dur;
+    a.dur_len = ctx->dur_len;
+    a.history_W = ctx->cfg.history_W;
+    a.window_K = ctx->cfg.window_K;
+    a.cand_inside = ctx->cfg.candidates == ASRKF_CAND_INSIDE;
     if (ctx->spill) {
         a.spill_min_D = ctx->cfg.spill_min_D;
         a.pool_rows = ctx->pool_rows;
@@ -711,18 +715,12 @@ asrkf_status decode_step_impl(asrkf_ctx* ctx, int32_t layer, const void* q, cons
     a.pool_rows = ctx->pool_rows;
     a.spill = ctx->spill ? 1 : 0;
     a.n_active = ctx->n_active + st0;
-    a.plen = ctx->plen;
-    a.unfreeze = ctx->unfreeze + st0 * ctx->cap;
-    a.count = ctx->count + st0 * ctx->cap;
-    a.hmask = ctx->hmask ? ctx->hmask + st0 * ctx->cap : nullptr;
-    a.hlast = ctx->hlast ? ctx->hlast + st0 * ctx->cap : nullptr;
-    a.history_W = c.history_W;
+    a.flag = ctx->flag + st0 * ctx->cap;
     a.rel_mode = c.relevance;
     a.scope_token = ctx->token_scope ? 1 : 0;
     a.first_layer = layer == 0 ? 1 : 0;
     a.rel_acc = ctx->rel_acc;
     a.xlog = ctx->xlog;
-    a.dur = ctx->dur;
     a.part_acc = ctx->part_acc;
     a.part_ml = ctx->part_ml;
     a.slot_first = ctx->slot_info;
@@ -738,10 +736,6 @@ asrkf_status decode_step_impl(asrkf_ctx* ctx, int32_t layer, const void* q, cons
     a.cap = ctx->cap;
     a.Hq = c.n_q_heads;
     a.Hkv = c.n_kv_heads;
-    a.t = t;
-    a.window_K = c.window_K;
-    a.cand_inside = c.candidates == ASRKF_CAND_INSIDE;
-    a.dur_len = ctx->dur_len;
     a.tau_H = c.tau * (float)c.n_q_heads;
     a.scale_log2 = (float)(1.4426950408889634 / sqrt((double)c.head_dim));
 
@@ -777,21 +771,11 @@ asrkf_status decode_step_impl(asrkf_ctx* ctx, int32_t layer, const void* q, cons
         r.norm = ctx->norm;
         r.list = a.list;
         r.n_active = a.n_active;
-        r.plen = ctx->plen;
-        r.unfreeze = a.unfreeze;
-        r.count = a.count;
-        r.hmask = a.hmask;
-        r.hlast = a.hlast;
-        r.dur = ctx->dur;
+        r.flag = a.flag;
         r.rel_acc = ctx->rel_acc;
         r.B = c.batch;
         r.cap = ctx->cap;
         r.Hq = c.n_q_heads;
-        r.t = t;
-        r.window_K = c.window_K;
-        r.cand_inside = a.cand_inside;
-        r.dur_len = ctx->dur_len;
-        r.history_W = c.history_W;
         r.scope_token = a.scope_token;
         r.first_layer = a.first_layer;
         r.tau_H = a.tau_H;
