@@ -41,6 +41,9 @@ def parse():
     ap.add_argument("--history-W", type=int, default=None, help="detection-count window (0 = all)")
     ap.add_argument("--candidates", choices=["outside", "inside"], default=None,
                     help="freeze candidates relative to the K-recent window (default: outside)")
+    ap.add_argument("--graph", action="store_true",
+                    help="time the steps as HIP graph replays: each timed step (every layer's "
+                         "decode_step and the restore) is captured beforehand as a graph")
     ap.add_argument("--layers", type=int, default=0,
                     help="run only the first N layers of the workload (counter runs); 0 = all")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",
@@ -219,6 +222,9 @@ def main():
         print(json.dumps(summarize_counters(*args.summarize_counters, args.steps,
                                             args.copy_calibration or (1 << 30)), indent=1))
         return
+    if args.graph and args.warmup < 1:
+        print("bench.py --graph needs at least one warm-up step before the capture", file=sys.stderr)
+        sys.exit(2)
     if args.gpus != 1:
         print(f"bench.py measures one GPU only: the library has no multi-GPU path "
               f"(asked for --gpus {args.gpus}).", file=sys.stderr)
@@ -280,6 +286,19 @@ def main():
         for t in range(1, W + 1):
             step(t)
         torch.cuda.synchronize()
+        if args.graph and not timing:
+            # every timed step captured beforehand as its own HIP graph (the same kernels,
+            # reading that step's inputs); the timed loop launches the graphs in order
+            graphs = []
+            for t in range(W + 1, W + K + 1):
+                g = torch.cuda.CUDAGraph()
+                with torch.cuda.graph(g):
+                    step(t)
+                graphs.append(g)
+            torch.cuda.synchronize()
+
+            def step(t):                                         # noqa: F811
+                graphs[t - W - 1].replay()
         A.asrkf_stats_reset(ctx)
         A.asrkf_set_timing(ctx, timing)
         torch.cuda.synchronize()
@@ -349,7 +368,7 @@ def main():
         "vs_baseline": None,
         "dtype": w.dtype,
         "data": "synthetic (seeded heavy-hitter generator, device twin)",
-        "config": {"workload": w.name, "layers": L, "batch": B, "context": w.prefill[0]
+        "config": {"workload": w.name, "graph": bool(args.graph), "layers": L, "batch": B, "context": w.prefill[0]
                    if len(set(w.prefill)) == 1 else "ragged", "q_heads": Hq, "kv_heads": Hkv,
                    "head_dim": D, "window_K": w.window_K, "tau": w.tau, "k": w.k_soft,
                    "vocab": w.vocab, "mode": "spill" if w.spill_min_D else "resident",

@@ -279,6 +279,9 @@ attention_kernel(AttnArgs a) {
     // the wave-state merge runs after the chunk loop: it reuses the chunk buffers
     float* merge_lds = reinterpret_cast<float*>(pos_lds);        // [kWaves/2][NV][64]
 
+    // the step's first launch advances the device step counter that the
+    // end-of-step rebuild reads (a graph replay of the step then sees its step)
+    if (a.t_dev && blockIdx.x == 0 && threadIdx.x == 0) *a.t_dev += 1;
     plan_ranges(a.n_active, a.B, seq_off);
     __syncthreads();
     const int T = wave_uniform(seq_off[a.B]);

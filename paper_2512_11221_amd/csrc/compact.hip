@@ -128,6 +128,29 @@ __device__ __forceinline__ void load_tile(const CompactArgs& a, size_t base, int
     }
 }
 
+// Every rebuild kernel starts here: the step index t comes from the device
+// counter that the step's first attention launch advanced (so a step captured
+// in a graph replays with the right index), the freeze loop runs from step 1
+// on, and the rebuild after a step that took a sequence past max_ctx positions
+// (a replayed step; the host refuses such a step otherwise) is refused: flag
+// for the host, nothing read or written, so every access stays below
+// max_ctx + 1 <= cap.  Returns n_t of sequence b, or -1 when refused.
+// Uniform over the workgroup.
+__device__ __forceinline__ int begin_rebuild(CompactArgs& a, int b, bool first_pass) {
+    a.t = *a.t_dev;
+    a.freeze = a.t > 0 ? 1 : 0;
+    const int n = a.plen[b] + a.t;
+    if (n > a.max_ctx) {
+        if (threadIdx.x == 0) a.flags[1] = 1;
+        return -1;
+    }
+    // a forced recovery level (no logits) is counted once per rebuild, by its first pass
+    if (first_pass && a.count_forced && a.forced_level > 0 && blockIdx.x == 0 && blockIdx.y == 0 &&
+        threadIdx.x == 0)
+        atomicAdd(a.recoveries + a.forced_level, (unsigned long long)a.B);
+    return n;
+}
+
 // Recovery select of one position.  Written with bitwise operators only: one
 // select per position, no short-circuit control flow.
 __device__ __forceinline__ int recover(const Ladder& r, int u, int q, bool live, bool& hit) {
@@ -240,7 +263,8 @@ compact_kernel(CompactArgs a) {
     __shared__ int tot0[kWaves], tot1[kWaves];
     const int inst = blockIdx.x;
     const int b = inst % a.B;
-    const int n = a.plen[b] + a.t;            // positions after step t
+    const int n = begin_rebuild(a, b, true);        // positions after step t
+    if (n < 0) return;
     const Ladder r = make_ladder(a, b, n);
     const size_t base = (size_t)inst * a.cap;
     const int listed = compact_range<0>(a, r, base, n, 0, n, 0, tot0, tot1);
@@ -255,7 +279,8 @@ compact_count_kernel(CompactArgs a) {
     __shared__ int tot0[kWaves], tot1[kWaves];
     const int seg = blockIdx.x, inst = blockIdx.y;
     const int b = inst % a.B;
-    const int n = a.plen[b] + a.t;
+    const int n = begin_rebuild(a, b, true);
+    if (n < 0) return;
     const int lo = seg * a.seg_len, hi = min(n, lo + a.seg_len);
     int cnt = 0;
     if (lo < hi) {
@@ -271,7 +296,8 @@ compact_write_kernel(CompactArgs a) {
     __shared__ int prefix;
     const int seg = blockIdx.x, inst = blockIdx.y;
     const int b = inst % a.B;
-    const int n = a.plen[b] + a.t;
+    const int n = begin_rebuild(a, b, false);
+    if (n < 0) return;
     const int lo = seg * a.seg_len, hi = min(n, lo + a.seg_len);
     const int last = n > 0 ? (n - 1) / a.seg_len : 0;
     if (seg > last) return;
@@ -296,7 +322,8 @@ compact_spill_kernel(CompactArgs a) {
 
     const int inst = blockIdx.x;
     const int b = inst % a.B;
-    const int n = a.plen[b] + a.t;
+    const int n = begin_rebuild(a, b, true);
+    if (n < 0) return;
     const Ladder r = make_ladder(a, b, n);
     const size_t base = (size_t)inst * a.cap;
     int32_t* U = a.unfreeze + base;
@@ -406,7 +433,7 @@ compact_spill_kernel(CompactArgs a) {
         listed += sc.tot0;
         popped += sc.tot1;
     }
-    if (short_of_rows) *a.overflow = 1;
+    if (short_of_rows) a.flags[0] = 1;
     __syncthreads();
     if (tid == 0) {
         const int restored = min(popped, top);
@@ -416,7 +443,7 @@ compact_spill_kernel(CompactArgs a) {
             dev = stack[idx];
             row_of[n] = dev;
         } else {
-            *a.overflow = 1;
+            a.flags[0] = 1;
         }
         list[listed] = n;
         lrow[listed] = dev;
@@ -460,7 +487,8 @@ spill_count_kernel(CompactArgs a) {
     __shared__ int tot0[kWaves], tot1[kWaves];
     const int seg = blockIdx.x, inst = blockIdx.y;
     const int b = inst % a.B;
-    const int n = a.plen[b] + a.t;
+    const int n = begin_rebuild(a, b, true);
+    if (n < 0) return;
     const int lo = seg * a.seg_len, hi = min(n, lo + a.seg_len);
     const Ladder r = make_ladder(a, b, n);
     const size_t base = (size_t)inst * a.cap;
@@ -514,7 +542,8 @@ spill_push_kernel(CompactArgs a) {
     __shared__ SegCounts pre;
     const int seg = blockIdx.x, inst = blockIdx.y;
     const int b = inst % a.B;
-    const int n = a.plen[b] + a.t;
+    const int n = begin_rebuild(a, b, false);
+    if (n < 0) return;
     const int lo = seg * a.seg_len, hi = min(n, lo + a.seg_len);
     if (lo >= hi) return;
     if (threadIdx.x == 0) pre = seg_prefix(a, inst, seg);
@@ -570,7 +599,8 @@ spill_list_kernel(CompactArgs a) {
     __shared__ SegCounts pre, all;
     const int seg = blockIdx.x, inst = blockIdx.y;
     const int b = inst % a.B;
-    const int n = a.plen[b] + a.t;
+    const int n = begin_rebuild(a, b, false);
+    if (n < 0) return;
     const int lo = seg * a.seg_len, hi = min(n, lo + a.seg_len);
     const int last = n > 0 ? (n - 1) / a.seg_len : 0;
     if (seg > last) return;
@@ -628,7 +658,7 @@ spill_list_kernel(CompactArgs a) {
         listed += sc.tot0;
         popped += sc.tot1;
     }
-    if (short_of_rows) *a.overflow = 1;
+    if (short_of_rows) a.flags[0] = 1;
     if (seg == last && threadIdx.x == 0) {
         const int idx = top - 1 - all.need;   // the next token's row
         int dev = 0;
@@ -636,7 +666,7 @@ spill_list_kernel(CompactArgs a) {
             dev = stack[idx];
             row_of[n] = dev;
         } else {
-            *a.overflow = 1;
+            a.flags[0] = 1;
         }
         a.list[base + all.flag] = n;
         a.list_row[base + all.flag] = dev;

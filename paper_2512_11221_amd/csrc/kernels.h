@@ -58,6 +58,7 @@ struct AttnArgs {
     uint8_t* flag;            // layer base, [B][cap]: 1 where the attended position scores
                               // below tau (Eq. 2), 0 where not; read by the freeze loop
                               // at the end of the step
+    int32_t* t_dev;           // first layer of a step: advanced by one (steps started), else null
     float* part_acc;          // [grid + B][Hq][D]
     float* part_ml;           // [grid + B][Hq][2]: (max in log2 units, sum)
     int32_t* slot_first;      // [B] first partial slot of each sequence (written)
@@ -108,7 +109,13 @@ struct CompactArgs {
     const int32_t* level;     // [B] recovery level per sequence (may be null)
     unsigned long long* listed_total;  // running sum of list lengths
     int32_t forced_level;     // -1: read level[]; 0: none; 1..3 forced SR/WR/FR
-    int32_t t;                // completed step; lists are built for step t+1
+    int32_t count_forced;     // 1: count a forced level (no logits) in recoveries[]
+    unsigned long long* recoveries;  // [4], indexed by level 1..3
+    const int32_t* t_dev;     // steps started (advanced by each step's first attention launch)
+    int32_t t;                // completed step, read from t_dev; lists are built for step t+1
+    int32_t max_ctx;          // positions per sequence; a rebuild that would pass it is refused
+    int32_t* flags;           // [0] a sequence ran out of device rows (spill mode),
+                              // [1] a step would pass max_ctx positions
     int32_t B, cap, wr_last_N;
     // spill mode only (spill_min_D > 0)
     int32_t spill_min_D;
@@ -124,10 +131,9 @@ struct CompactArgs {
     int32_t* in_pos;          // [L][B][cap] rows to copy back: position ...
     int32_t* in_row;          //   ... and the device row it takes
     int32_t* n_in;            // [L][B]
-    int32_t* overflow;        // set to 1 when a sequence needs more device rows than it has
     unsigned long long* xfer; // [0] rows to host, [1] rows from host, [2] device rows released
     // the freeze loop of step t runs here, before recovery (not before step 1)
-    int32_t freeze;           // 1: apply the step's freeze loop
+    int32_t freeze;           // 1: apply the step's freeze loop (set on the device: t > 0)
     const uint8_t* flag;      // [L][B][cap] layer scope: 1 where the position scored below tau at step t
     int32_t scope_token;      // 1: one state per sequence, scored by the sum over layers
     const float* rel_acc;     // [B][cap] token scope: relevance summed over layers and heads

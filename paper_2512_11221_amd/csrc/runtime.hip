@@ -145,15 +145,16 @@ struct asrkf_ctx {
     int32_t* in_pos = nullptr;
     int32_t* in_row = nullptr;
     int32_t* n_in = nullptr;
-    int32_t* overflow = nullptr;
+    int32_t* flags = nullptr;     // [0] out of device rows (spill), [1] past max_ctx (device check)
+    int32_t* t_dev = nullptr;     // steps started, advanced by each step's first attention launch
     void* khost = nullptr;        // pinned host store (host pointers)
     void* vhost = nullptr;
     void* khost_dev = nullptr;    // the same memory as seen by kernels
     void* vhost_dev = nullptr;
-    int32_t* overflow_host = nullptr;   // pinned copy of *overflow
+    int32_t* flags_host = nullptr;      // pinned copy of flags (spill mode, read without a wait)
     hipStream_t side = nullptr;   // copies to and from the host store
     hipEvent_t ev_lists = nullptr;      // compaction done (main stream)
-    hipEvent_t ev_flag = nullptr;       // overflow flag copied to the host
+    hipEvent_t ev_flag = nullptr;       // flags copied to the host
     std::vector<hipEvent_t> ev_in;      // per layer: its restores are in the device cache
     bool xfer_recorded = false;
     bool flag_recorded = false;
@@ -171,7 +172,6 @@ struct asrkf_ctx {
     std::vector<std::pair<hipEvent_t, hipEvent_t>> ev_used, ev_free;
     double attn_ms_done = 0.0;
     int64_t attn_launches = 0;
-    int64_t host_recoveries[4] = {0, 0, 0, 0};
     int side_delay_us = 0;              // test hook: side stream waits before its copies
     int device = 0;
     void* static_scratch = nullptr;     // this device's address of the static partials array
@@ -224,10 +224,10 @@ void free_all(asrkf_ctx* ctx) {
                     ctx->entropy, ctx->pmax, ctx->part_acc, ctx->part_ml, ctx->slot_info, ctx->ent_partial, ctx->ent_ticket,
                     ctx->counters, ctx->row_of, ctx->on_host, ctx->list_row, ctx->free_rows,
                     ctx->free_top, ctx->out_pos, ctx->out_row, ctx->n_out, ctx->in_pos, ctx->in_row,
-                    ctx->n_in, ctx->overflow, ctx->hmask, ctx->hlast, ctx->rel_acc, ctx->xlog,
+                    ctx->n_in, ctx->flags, ctx->t_dev, ctx->hmask, ctx->hlast, ctx->rel_acc, ctx->xlog,
                     ctx->norm, ctx->seg_count};
     for (void* p : ptrs) if (p) (void)hipFree(p);
-    void* host[] = {ctx->khost, ctx->vhost, ctx->overflow_host};
+    void* host[] = {ctx->khost, ctx->vhost, ctx->flags_host};
     for (void* p : host) if (p) (void)hipHostFree(p);
     if (ctx->side) (void)hipStreamDestroy(ctx->side);
     if (ctx->ev_lists) (void)hipEventDestroy(ctx->ev_lists);
@@ -292,8 +292,14 @@ bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15) == 
 // The context's arrays (cache, token states, lists, split partials) are shared
 // by every call, so a call on another stream than the previous one first waits
 // for everything that call queued.
+bool capturing(hipStream_t s) {
+    hipStreamCaptureStatus st = hipStreamCaptureStatusNone;
+    return hipStreamIsCapturing(s, &st) == hipSuccess && st == hipStreamCaptureStatusActive;
+}
+
 hipError_t follow_last_stream(asrkf_ctx* ctx, hipStream_t s) {
-    if (!ctx->queued || s == ctx->last_stream) return hipSuccess;
+    // under stream capture the caller orders the capture after earlier work
+    if (!ctx->queued || s == ctx->last_stream || capturing(s)) return hipSuccess;
     hipError_t e = hipEventRecord(ctx->ev_switch, ctx->last_stream);
     if (e == hipSuccess) e = hipStreamWaitEvent(s, ctx->ev_switch, 0);
     return e;
@@ -411,6 +417,8 @@ asrkf_status asrkf_init(const asrkf_config* cfg, asrkf_ctx** out) {
     ALLOC(ent_partial, (size_t)c.batch * kEntropySplitMax * 3 * 4);
     ALLOC(ent_ticket, (size_t)c.batch * 4);
     ALLOC(counters, kCounters * sizeof(unsigned long long));
+    ALLOC(flags, 8);
+    ALLOC(t_dev, 4);
     if (ctx->spill) {
         ALLOC(row_of, per_pos * 4);
         ALLOC(on_host, per_pos);
@@ -423,20 +431,19 @@ asrkf_status asrkf_init(const asrkf_config* cfg, asrkf_ctx** out) {
         ALLOC(in_pos, per_pos * 4);
         ALLOC(in_row, per_pos * 4);
         ALLOC(n_in, inst * 4);
-        ALLOC(overflow, 4);
         // host store: pinned, mapped, coarse-grained (only the GPU reads and writes it)
         const size_t store = per_pos * ctx->row_bytes;
         const unsigned flags = hipHostMallocMapped | hipHostMallocNonCoherent;
         hipError_t he = hipHostMalloc(&ctx->khost, store, flags);
         if (he == hipSuccess) he = hipHostMalloc(&ctx->vhost, store, flags);
-        if (he == hipSuccess) he = hipHostMalloc((void**)&ctx->overflow_host, 64, hipHostMallocDefault);
+        if (he == hipSuccess) he = hipHostMalloc((void**)&ctx->flags_host, 64, hipHostMallocDefault);
         if (he != hipSuccess) {
             (void)hipGetLastError();
             free_all(ctx);
             delete ctx;
             return fail(ASRKF_ENOMEM, "pinned host store of 2 x %zu bytes: %s", store, hipGetErrorString(he));
         }
-        *ctx->overflow_host = 0;
+        ctx->flags_host[0] = ctx->flags_host[1] = 0;
         he = hipHostGetDevicePointer(&ctx->khost_dev, ctx->khost, 0);
         if (he == hipSuccess) he = hipHostGetDevicePointer(&ctx->vhost_dev, ctx->vhost, 0);
         if (he == hipSuccess) he = hipStreamCreateWithFlags(&ctx->side, hipStreamNonBlocking);
@@ -483,7 +490,8 @@ asrkf_status asrkf_init(const asrkf_config* cfg, asrkf_ctx** out) {
     INIT(hipMemset(ctx->pmax, 0, (size_t)c.batch * 4));
     INIT(hipMemset(ctx->ent_ticket, 0, (size_t)c.batch * 4));
     INIT(hipMemset(ctx->counters, 0, kCounters * sizeof(unsigned long long)));
-    if (ctx->spill) INIT(hipMemset(ctx->overflow, 0, 4));
+    INIT(hipMemset(ctx->flags, 0, 8));
+    INIT(hipMemset(ctx->t_dev, 0, 4));
     INIT(hipMemcpy(ctx->dur, table.data(), table.size() * 4, hipMemcpyHostToDevice));
     INIT(hipDeviceSynchronize());
 #undef INIT
@@ -551,15 +559,18 @@ asrkf_status build_lists(asrkf_ctx* ctx, int forced_level, hipStream_t s) {
     a.level = ctx->level;
     a.listed_total = ctx->counters;
     a.forced_level = forced_level;
-    a.t = ctx->t;
+    a.count_forced = forced_level > 0 ? 1 : 0;       // no logits: the entropy kernel counts none
+    a.recoveries = ctx->counters;
+    a.t_dev = ctx->t_dev;
+    a.max_ctx = ctx->cfg.max_ctx;
+    a.flags = ctx->flags;
     a.B = ctx->cfg.batch;
     a.cap = ctx->cap;
     a.wr_last_N = ctx->cfg.wr_last_N;
     a.n_seg = ctx->n_seg;
     a.seg_len = ctx->seg_len;
     a.seg_count = ctx->seg_count;
-    // the freeze loop of the step that ends here (there is none before the first step)
-    a.freeze = ctx->t > 0 ? 1 : 0;
+    // the freeze loop of the step that ends here (the kernels skip it before step 1)
     a.flag = ctx->flag;
     a.scope_token = ctx->token_scope ? 1 : 0;
     a.rel_acc = ctx->rel_acc;
@@ -586,14 +597,13 @@ asrkf_status build_lists(asrkf_ctx* ctx, int forced_level, hipStream_t s) {
         a.in_pos = ctx->in_pos;
         a.in_row = ctx->in_row;
         a.n_in = ctx->n_in;
-        a.overflow = ctx->overflow;
         a.xfer = ctx->counters + 8;
     }
     HIP_OK(ctx, launch_compact(a, n_inst, s));
     if (!ctx->spill) return ASRKF_OK;
 
     // the flag tells the host (one step late, without a wait) that rows ran out
-    HIP_OK(ctx, hipMemcpyAsync(ctx->overflow_host, ctx->overflow, 4, hipMemcpyDeviceToHost, s));
+    HIP_OK(ctx, hipMemcpyAsync(ctx->flags_host, ctx->flags, 8, hipMemcpyDeviceToHost, s));
     HIP_OK(ctx, hipEventRecord(ctx->ev_flag, s));
     ctx->flag_recorded = true;
 
@@ -630,20 +640,32 @@ asrkf_status build_lists(asrkf_ctx* ctx, int forced_level, hipStream_t s) {
     return ASRKF_OK;
 }
 
-// Spill mode: a sequence ran out of device rows at an earlier step.  Checked
-// without waiting (the flag copy of the last rebuild may still be queued) or,
-// from the synchronizing calls, after a full wait.
+// The device flags of earlier rebuilds: a sequence ran out of device rows
+// (spill mode), or a step would have passed max_ctx positions (a step replayed
+// from a graph, which the host checks do not see).  Without waiting, only spill
+// mode's flag copy is read, if it has arrived; the synchronizing calls read the
+// flags themselves after their wait.
 asrkf_status check_overflow(asrkf_ctx* ctx, bool synced) {
-    if (!ctx->spill || !ctx->flag_recorded) return ASRKF_OK;
-    if (!synced) {
+    int32_t f[2] = {0, 0};
+    if (synced) {
+        HIP_OK(ctx, hipMemcpy(f, ctx->flags, 8, hipMemcpyDeviceToHost));
+    } else {
+        if (!ctx->spill || !ctx->flag_recorded) return ASRKF_OK;
         const hipError_t q = hipEventQuery(ctx->ev_flag);
         if (q == hipErrorNotReady) return ASRKF_OK;
         if (q != hipSuccess) return hip_fail(ctx, q, "hipEventQuery");
+        f[0] = ((volatile int32_t*)ctx->flags_host)[0];
+        f[1] = ((volatile int32_t*)ctx->flags_host)[1];
     }
-    if (*(volatile int32_t*)ctx->overflow_host) {
+    if (f[0]) {
         ctx->poisoned = true;
         return fail(ASRKF_ECAPACITY, "a sequence needed more than device_rows = %d device rows; "
                     "results since then are void", ctx->pool_rows);
+    }
+    if (f[1]) {
+        ctx->poisoned = true;
+        return fail(ASRKF_ECAPACITY, "a replayed step would pass max_ctx = %d positions; the "
+                    "active caches were not rebuilt since then", ctx->cfg.max_ctx);
     }
     return ASRKF_OK;
 }
@@ -682,9 +704,13 @@ asrkf_status decode_step_impl(asrkf_ctx* ctx, int32_t layer, const void* q, cons
     for (int b = 0; b < c.batch; ++b)
         if (ctx->plen_host[b] + t > c.max_ctx)
             return fail(ASRKF_ECAPACITY, "sequence %d would exceed max_ctx=%d", b, c.max_ctx);
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    const bool capture = capturing(s);
+    if (capture && (ctx->spill || !ctx->lists_ready))
+        return fail(ASRKF_ESTATE, ctx->spill ? "spill-mode steps cannot be captured in a graph"
+                                             : "capture a step only after the first decode step");
     st = check_overflow(ctx, false);
     if (st != ASRKF_OK) return st;
-    hipStream_t s = static_cast<hipStream_t>(stream);
     HIP_OK(ctx, follow_last_stream(ctx, s));
     mark_queued(ctx, s);
     if (!ctx->lists_ready) {
@@ -716,6 +742,7 @@ asrkf_status decode_step_impl(asrkf_ctx* ctx, int32_t layer, const void* q, cons
     a.spill = ctx->spill ? 1 : 0;
     a.n_active = ctx->n_active + st0;
     a.flag = ctx->flag + st0 * ctx->cap;
+    a.t_dev = layer == 0 ? ctx->t_dev : nullptr;
     a.rel_mode = c.relevance;
     a.scope_token = ctx->token_scope ? 1 : 0;
     a.first_layer = layer == 0 ? 1 : 0;
@@ -740,7 +767,7 @@ asrkf_status decode_step_impl(asrkf_ctx* ctx, int32_t layer, const void* q, cons
     a.scale_log2 = (float)(1.4426950408889634 / sqrt((double)c.head_dim));
 
     std::pair<hipEvent_t, hipEvent_t> ev{nullptr, nullptr};
-    if (ctx->timing && !use_static) {
+    if (ctx->timing && !use_static && !capture) {
         if (!ctx->ev_free.empty()) {
             ev = ctx->ev_free.back();
             ctx->ev_free.pop_back();
@@ -812,9 +839,10 @@ asrkf_status asrkf_restore(asrkf_ctx* ctx, const float* logits, int32_t mode, vo
     if (ctx->next_layer != c.n_layers)
         return fail(ASRKF_ESTATE, "restore before decode_step of every layer (next layer %d of %d)",
                     ctx->next_layer, c.n_layers);
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    if (ctx->spill && capturing(s)) return fail(ASRKF_ESTATE, "spill-mode steps cannot be captured in a graph");
     st = check_overflow(ctx, false);
     if (st != ASRKF_OK) return st;
-    hipStream_t s = static_cast<hipStream_t>(stream);
     HIP_OK(ctx, follow_last_stream(ctx, s));
     mark_queued(ctx, s);
     int forced;
@@ -839,9 +867,10 @@ asrkf_status asrkf_restore(asrkf_ctx* ctx, const float* logits, int32_t mode, vo
         forced = -1;                           // level[] written by the entropy kernel
     } else {
         forced = (mode >= ASRKF_SR && mode <= ASRKF_FR) ? (int)mode : 0;
-        if (forced) ctx->host_recoveries[forced] += c.batch;
     }
-    ctx->t += 1;
+    // a captured step runs only when replayed: the host learns of it from the
+    // device step counter at its next wait
+    if (!capturing(s)) ctx->t += 1;
     ctx->next_layer = 0;
     return build_lists(ctx, forced, s);
 }
@@ -853,9 +882,16 @@ namespace {
 // Everything the context queued: its calls are ordered on last_stream (a call
 // on a new stream waits for the previous one), except the spill-mode copies
 // on the side stream, which the next decode_step waits for.
+// Steps replayed from a captured graph advance only the device's step
+// counter: after the wait the host adopts it (the counter counts steps
+// started, so a step in progress is not yet complete).
 asrkf_status sync_ctx(asrkf_ctx* ctx) {
     HIP_OK(ctx, hipStreamSynchronize(ctx->last_stream));
     if (ctx->side) HIP_OK(ctx, hipStreamSynchronize(ctx->side));
+    int32_t started = 0;
+    HIP_OK(ctx, hipMemcpy(&started, ctx->t_dev, 4, hipMemcpyDeviceToHost));
+    const int completed = started - (ctx->next_layer != 0 ? 1 : 0);
+    if (completed > ctx->t) ctx->t = completed;
     return ASRKF_OK;
 }
 
@@ -907,7 +943,7 @@ asrkf_status asrkf_stats(asrkf_ctx* ctx, asrkf_stats_t* out) {
     out->total_positions = total;
     out->active_positions = active;
     out->attended_total = ctx->lists_ready ? (int64_t)cnt[0] * per_list - current : 0;
-    for (int i = 1; i < 4; ++i) out->recoveries[i] = (int64_t)cnt[i] + ctx->host_recoveries[i];
+    for (int i = 1; i < 4; ++i) out->recoveries[i] = (int64_t)cnt[i];
     out->rr_requests = (int64_t)cnt[5];
     out->attn_launches = ctx->attn_launches;
     out->attn_kernel_ms = ctx->attn_ms_done;
@@ -934,7 +970,6 @@ asrkf_status asrkf_stats_reset(asrkf_ctx* ctx) {
     if (ctx->lists_ready)
         for (size_t i = 0; i < inst; ++i) cnt[0] += (unsigned long long)na[i];
     HIP_OK(ctx, hipMemcpy(ctx->counters, cnt, sizeof cnt, hipMemcpyHostToDevice));
-    for (int i = 0; i < 4; ++i) ctx->host_recoveries[i] = 0;
     ctx->attn_ms_done = 0.0;
     ctx->attn_launches = 0;
     return ASRKF_OK;
