@@ -28,6 +28,17 @@
  *    the work that call queued (the context's cache, states and scratch are
  *    shared by all calls).  Calls marked "waits" synchronize only the
  *    context's own streams, not the whole device.
+ *  - Graph capture (resident mode): after the first decode step, a whole step
+ *    (decode_step of every layer, then restore) may be captured on a stream
+ *    into a HIP graph and replayed; the kernels take the step index from the
+ *    context's device counter, so each replay runs the next step.  A captured
+ *    call queues nothing until the graph is replayed.  The host learns of
+ *    replayed steps at its next waiting call (asrkf_stats, asrkf_get_state,
+ *    ...), which the caller makes before any further uncaptured decode_step.
+ *    A replayed step that takes a sequence past max_ctx positions is caught
+ *    on the device (the end-of-step rebuild is skipped, no access goes out
+ *    of bounds) and reported as ECAPACITY by the next waiting call.  Capture
+ *    returns ESTATE before the first decode step and in spill mode.
  *  - On any HIP runtime error the context is poisoned: that call returns
  *    ASRKF_EHIP and every later call returns ASRKF_ESTATE until destroy.
  *    asrkf_last_error() gives a message for the calling thread.
