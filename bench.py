@@ -403,6 +403,7 @@ def main():
         row = bytes_per_token // 2                      # one K or V row
         line["spill"] = {"spill_min_D": w.spill_min_D, "rows_to_host": st["rows_to_host"],
                          "rows_from_host": st["rows_from_host"],
+                         "rows_reused": st["rows_reused"],
                          "h2d_GBps": 2 * row * st["rows_from_host"] / elapsed / 1e9,
                          "d2h_GBps": 2 * row * st["rows_to_host"] / elapsed / 1e9}
     if args.cpu_seconds > 0:

@@ -146,6 +146,8 @@ typedef struct {
                                    host store (each token at most once per layer) */
     int64_t rows_from_host;     /* spill mode: token rows copied back to the device */
     int64_t rows_released;      /* spill mode: device rows given up by freezing tokens */
+    int64_t rows_reused;        /* spill mode: restored tokens that took back their last device
+                                   row, which still held their K and V (no copy) */
 } asrkf_stats_t;
 
 typedef struct asrkf_ctx asrkf_ctx;

@@ -47,6 +47,7 @@ class asrkf_stats_t(ctypes.Structure):
         ("attn_launches", ctypes.c_int64), ("attn_kernel_ms", ctypes.c_double),
         ("compression", ctypes.c_double), ("rows_to_host", ctypes.c_int64),
         ("rows_from_host", ctypes.c_int64), ("rows_released", ctypes.c_int64),
+        ("rows_reused", ctypes.c_int64),
     ]
 
     def as_dict(self):

@@ -22,16 +22,18 @@
 //
 // Spill mode (Sec. 3.2: frozen KV leaves the GPU) adds device-row bookkeeping
 // to the same pass structure, all of it on the device:
-//   pass 1  a token frozen at step t for d >= spill_min_D steps gives its
-//           device row back to the sequence's free stack; if the host store
-//           does not hold its rows yet (K and V never change, so they are
-//           copied out once), the (position, row) pair goes to the out-list;
-//   pass 2  every position of the new active list that has no device row
-//           (its timer ran out, or recovery released it) takes one from the
-//           stack and goes to the in-list; the next token takes one too.
-// Rows are pushed and popped in ascending position order, so the assignment
-// is the same on every run.  The copies themselves are made by the transfer
-// kernel (out-list first, so a row is read before it is handed out again).
+//   pass 1  a token frozen at step t for d >= spill_min_D steps gives up its
+//           device row; if the host store does not hold its rows yet (K and V
+//           never change, so they are copied out once), the (position, row)
+//           pair goes to the out-list.  A position of the new active list
+//           without a device row takes its last row back when that row still
+//           holds its K/V;
+//   rows    the positions still without a row, and the next token, take free
+//           rows found by a search that wraps around the rows;
+//   pass 2  the list of the next step and the row of every entry; positions
+//           that took a found row go to the in-list.
+// The copies themselves are made by the transfer kernel (out-list first, so a
+// row is read before it is handed out again).
 //
 // The in-order compaction uses wave ballots: every thread owns 4 consecutive
 // positions (one 16-byte load), mbcnt over 4 ballots gives the exclusive
@@ -316,9 +318,170 @@ compact_write_kernel(CompactArgs a) {
     if (seg == last && threadIdx.x == 0) finish_list(a, inst, base, n, prefix + cnt);
 }
 
+// ---- spill mode ----
+// A token frozen at step t for d >= spill_min_D steps gives up its device row
+// (row_of = -1; last_row remembers the row).  The row is then free, but it keeps
+// the token's K/V until another position is written into it: every row records
+// its owner, the position whose K/V it holds, and is free unless that owner
+// currently sits in it,
+//     free(r) = owner[r] < 0 || row_of[owner[r]] != r.
+// A host-only position that attends again takes its last row back when the row
+// still holds its K/V (no copy), else a free row that a search finds, and its
+// K/V comes back from the host store.  The search starts where the previous
+// one stopped and wraps around the rows, so a released row is handed out again
+// as late as the free rows allow.  Every decision is taken in ascending
+// position or row order, so the assignment is the same on every run.
+
+__device__ __forceinline__ bool row_free(const int32_t* owner, const int32_t* row_of, int r) {
+    const int o = owner[r];
+    return o < 0 || row_of[o] != r;
+}
+
+// Releases, out-list entries and take-backs of the positions p .. p+3 of a
+// thread (recovery already applied to u): released[k] for tokens frozen now
+// for d >= spill_min_D that still hold a row (first[k]: the host store does not
+// hold them yet), need[k] for listed positions without a row after the
+// take-backs, back[k] for the take-backs.  Writes row_of, last_row, on_host.
+struct SpillFlags {
+    bool released[4], first[4], need[4], back[4], listed[4];
+    int row[4];
+};
+
+__device__ __forceinline__ void spill_decide(const CompactArgs& a, const Ladder& r, size_t base,
+                                             int p, int hi, const int (&u)[4], SpillFlags& f) {
+    int32_t* row_of = a.row_of + base;
+    int32_t* last_row = a.last_row + base;
+    const int32_t* owner = a.row_owner + (base / a.cap) * a.pool_rows;
+    int row[4];
+    load4(row_of, p, hi, row, -1);
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+        const bool live = p + k < hi;
+        f.listed[k] = live & (u[k] <= r.t1);
+        // frozen at step t (U = t + d) for d >= spill_min_D, and still in a device row
+        f.released[k] = live & (row[k] >= 0) & (u[k] > r.t1) & (u[k] - a.t >= a.spill_min_D);
+        const bool stored = live ? a.on_host[base + p + k] != 0 : true;
+        f.first[k] = f.released[k] & !stored;
+        f.back[k] = false;
+        if (f.released[k]) {
+            row_of[p + k] = -1;
+            last_row[p + k] = row[k];
+            if (f.first[k]) a.on_host[base + p + k] = 1;
+            row[k] = -1;
+        } else if (f.listed[k] && row[k] < 0) {
+            const int lr = last_row[p + k];
+            if (lr >= 0 && owner[lr] == p + k) {           // its K/V is still in its last row
+                row_of[p + k] = lr;
+                row[k] = lr;
+                f.back[k] = true;
+            }
+        }
+        f.need[k] = f.listed[k] & (row[k] < 0);
+        f.row[k] = row[k];
+    }
+}
+
+// The first `need` free rows from the instance's hand on, in cyclic row order,
+// into pop_buf[0 .. need); returns how many there were (fewer when the rows ran
+// out) and moves the hand past the last one taken.  Every thread of the block
+// calls it.
+__device__ int find_free_rows(const CompactArgs& a, int inst, int need, int* tot0, int* tot1,
+                              int* last_idx) {
+    const int R = a.pool_rows;
+    const int32_t* owner = a.row_owner + (size_t)inst * R;
+    const int32_t* row_of = a.row_of + (size_t)inst * a.cap;
+    int32_t* pop = a.pop_buf + (size_t)inst * R;
+    const int h0 = a.hand[inst];
+    int found = 0;
+    if (threadIdx.x == 0) *last_idx = -1;
+    for (int s0 = 0; s0 < R && found < need; s0 += 4 * kThreads) {
+        bool f[4];
+        int rw[4];
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+            const int i = s0 + 4 * threadIdx.x + k;
+            rw[k] = (h0 + i) % R;
+            f[k] = i < R && row_free(owner, row_of, rw[k]);
+        }
+        int before, mine;
+        ballot4(f, before, mine);
+        const Scan sc = tile_scan(before, mine, 0, 0, tot0, tot1);
+        int slot = found + sc.off0;
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+            if (!f[k]) continue;
+            if (slot < need) pop[slot] = rw[k];
+            if (slot == need - 1) *last_idx = s0 + 4 * threadIdx.x + k;
+            ++slot;
+        }
+        found += sc.tot0;
+    }
+    __syncthreads();                          // last_idx; every thread has read the hand
+    if (threadIdx.x == 0 && *last_idx >= 0) a.hand[inst] = (h0 + *last_idx + 1) % R;
+    return min(found, need);
+}
+
+// The list of step t+1 for positions p .. p+3, with the device row of each;
+// listed positions that need a row take pop_buf[pn], pn counting up (their K/V
+// comes back from the host store: in-list).
+__device__ __forceinline__ void spill_list4(const CompactArgs& a, size_t base, int inst, int p,
+                                            const SpillFlags& f, int pl, int pn, int popped,
+                                            bool& short_of_rows) {
+    int32_t* owner = a.row_owner + (size_t)inst * a.pool_rows;
+    const int32_t* pop = a.pop_buf + (size_t)inst * a.pool_rows;
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+        if (!f.listed[k]) continue;
+        int dev = f.row[k];
+        if (f.need[k]) {
+            if (pn < popped) {
+                dev = pop[pn];
+                a.row_of[base + p + k] = dev;
+                owner[dev] = p + k;
+                a.in_pos[base + pn] = p + k;
+                a.in_row[base + pn] = dev;
+            } else {
+                dev = 0;                      // no row left: results are void, the host is told
+                short_of_rows = true;
+            }
+            ++pn;
+        }
+        a.list[base + pl] = p + k;
+        a.list_row[base + pl] = dev;
+        ++pl;
+    }
+}
+
+// The list tail: the next token's position n and the row it takes (the last
+// row found); counts and counters of the rebuild.
+__device__ __forceinline__ void spill_tail(const CompactArgs& a, int inst, size_t base, int n,
+                                           int listed, int need, int popped, int n_out,
+                                           int released, int back) {
+    int dev = 0;
+    if (need < popped) {
+        dev = a.pop_buf[(size_t)inst * a.pool_rows + need];
+        a.row_of[base + n] = dev;
+        a.row_owner[(size_t)inst * a.pool_rows + dev] = n;
+    } else {
+        a.flags[0] = 1;
+    }
+    a.list[base + listed] = n;
+    a.list_row[base + listed] = dev;
+    const int restored = min(need, popped);
+    a.n_out[inst] = n_out;
+    a.n_in[inst] = restored;
+    a.n_active[inst] = listed + 1;
+    atomicAdd(a.listed_total, (unsigned long long)(listed + 1));
+    if (n_out) atomicAdd(a.xfer + 0, (unsigned long long)n_out);
+    if (restored) atomicAdd(a.xfer + 1, (unsigned long long)restored);
+    if (released) atomicAdd(a.xfer + 2, (unsigned long long)released);
+    if (back) atomicAdd(a.xfer + 3, (unsigned long long)back);
+}
+
 __global__ void __launch_bounds__(kThreads)
 compact_spill_kernel(CompactArgs a) {
     __shared__ int tot0[kWaves], tot1[kWaves];
+    __shared__ int last_idx;
 
     const int inst = blockIdx.x;
     const int b = inst % a.B;
@@ -327,157 +490,106 @@ compact_spill_kernel(CompactArgs a) {
     const Ladder r = make_ladder(a, b, n);
     const size_t base = (size_t)inst * a.cap;
     int32_t* U = a.unfreeze + base;
-    int32_t* list = a.list + base;
-    int32_t* lrow = a.list_row + base;
-    int32_t* row_of = a.row_of + base;
-    uint8_t* on_host = a.on_host + base;
-    int32_t* stack = a.free_rows + (size_t)inst * a.pool_rows;
-    int32_t* out_pos = a.out_pos + base;
-    int32_t* out_row = a.out_row + base;
-    int32_t* in_pos = a.in_pos + base;
-    int32_t* in_row = a.in_row + base;
     const int tid = threadIdx.x;
-    const int top0 = a.free_top[inst];
 
-    // pass 1: the freeze loop and recovery, then release the rows of tokens
-    // frozen now for d >= spill_min_D
-    int pushed = 0, n_out = 0;
+    // pass 1: the freeze loop, recovery, releases (out-list), take-backs, and the
+    // number of positions that need a row
+    int n_out = 0, released = 0, back = 0, need = 0;
     for (int p0 = 0; p0 < n; p0 += 4 * kThreads) {
         const int p = p0 + 4 * tid;
         Tile4 cur;
         load_tile(a, base, p, n, cur);
         int (&u)[4] = cur.u;
-        int row[4];
-        load4(row_of, p, n, row, -1);
-        bool spill[4], first[4];
         bool dirty = freeze4(a, base, p, n, n, u, cur.c, cur.f);
 #pragma unroll
         for (int k = 0; k < 4; ++k) {
             bool hit;
-            const bool live = p + k < n;
-            u[k] = recover(r, u[k], p + k, live, hit);
+            u[k] = recover(r, u[k], p + k, p + k < n, hit);
             dirty |= hit;
-            // frozen at step t (U = t + d) for d >= spill_min_D, and still in a device row
-            spill[k] = live & (row[k] >= 0) & (u[k] > r.t1) & (u[k] - a.t >= a.spill_min_D);
-            const bool stored = live ? on_host[p + k] != 0 : true;
-            first[k] = spill[k] & !stored;
         }
         if (dirty) {
             for (int k = 0; k < 4; ++k) if (p + k < n) U[p + k] = u[k];
         }
+        SpillFlags f;
+        spill_decide(a, r, base, p, n, u, f);
         int b0, m0, b1, m1;
-        ballot4(spill, b0, m0);
-        ballot4(first, b1, m1);
-        const Scan sc = tile_scan(b0, m0, b1, m1, tot0, tot1);
-        int ps = top0 + pushed + sc.off0, po = n_out + sc.off1;
+        ballot4(f.first, b0, m0);
+        ballot4(f.released, b1, m1);
+        const Scan s1 = tile_scan(b0, m0, b1, m1, tot0, tot1);
+        int po = n_out + s1.off0;
 #pragma unroll
         for (int k = 0; k < 4; ++k) {
-            if (first[k]) {
-                out_pos[po] = p + k;
-                out_row[po] = row[k];
-                on_host[p + k] = 1;
-                ++po;
-            }
-            if (spill[k]) {
-                if (ps < a.pool_rows) stack[ps] = row[k];
-                row_of[p + k] = -1;
-                ++ps;
-            }
+            if (!f.first[k]) continue;
+            a.out_pos[base + po] = p + k;
+            a.out_row[base + po] = a.last_row[base + p + k];
+            ++po;
         }
-        pushed += sc.tot0;
-        n_out += sc.tot1;
+        ballot4(f.need, b0, m0);
+        ballot4(f.back, b1, m1);
+        const Scan s2 = tile_scan(b0, m0, b1, m1, tot0, tot1);
+        n_out += s1.tot0;
+        released += s1.tot1;
+        need += s2.tot0;
+        back += s2.tot1;
     }
-    __syncthreads();                          // stack and row_of writes are read below
-    const int top = min(a.pool_rows, top0 + pushed);
+    __syncthreads();                          // row_of and last_row writes are read below
 
-    // pass 2: the active list of step t+1, device rows for positions that lack one
-    int listed = 0, popped = 0;
+    // the rows for the positions that need one, and one for the next token
+    const int popped = find_free_rows(a, inst, need + 1, tot0, tot1, &last_idx);
+
+    // pass 2: the active list of step t+1 and the device row of every entry
+    int listed = 0, pn_run = 0;
     bool short_of_rows = false;
     for (int p0 = 0; p0 < n; p0 += 4 * kThreads) {
         const int p = p0 + 4 * tid;
-        int u[4], row[4];
+        int u[4];
         load4(U, p, n, u, 0);
-        load4(row_of, p, n, row, -1);
-        bool flag[4], need[4];
+        SpillFlags f;
+        int row[4];
+        load4(a.row_of + base, p, n, row, -1);
 #pragma unroll
         for (int k = 0; k < 4; ++k) {
-            flag[k] = (p + k < n) & (u[k] <= r.t1);
-            need[k] = flag[k] & (row[k] < 0);
+            f.listed[k] = (p + k < n) & (u[k] <= r.t1);
+            f.need[k] = f.listed[k] & (row[k] < 0);
+            f.row[k] = row[k];
         }
         int b0, m0, b1, m1;
-        ballot4(flag, b0, m0);
-        ballot4(need, b1, m1);
+        ballot4(f.listed, b0, m0);
+        ballot4(f.need, b1, m1);
         const Scan sc = tile_scan(b0, m0, b1, m1, tot0, tot1);
-        int pl = listed + sc.off0, pn = popped + sc.off1;
-#pragma unroll
-        for (int k = 0; k < 4; ++k) {
-            if (!flag[k]) continue;
-            int dev = row[k];
-            if (need[k]) {
-                const int idx = top - 1 - pn;
-                if (idx >= 0) {
-                    dev = stack[idx];
-                    row_of[p + k] = dev;
-                    in_pos[pn] = p + k;
-                    in_row[pn] = dev;
-                } else {
-                    dev = 0;                  // no row left: results are void, the host is told
-                    short_of_rows = true;
-                }
-                ++pn;
-            }
-            list[pl] = p + k;
-            lrow[pl] = dev;
-            ++pl;
-        }
+        spill_list4(a, base, inst, p, f, listed + sc.off0, pn_run + sc.off1, popped, short_of_rows);
         listed += sc.tot0;
-        popped += sc.tot1;
+        pn_run += sc.tot1;
     }
     if (short_of_rows) a.flags[0] = 1;
     __syncthreads();
-    if (tid == 0) {
-        const int restored = min(popped, top);
-        const int idx = top - 1 - popped;     // the next token's row
-        int dev = 0;
-        if (idx >= 0) {
-            dev = stack[idx];
-            row_of[n] = dev;
-        } else {
-            a.flags[0] = 1;
-        }
-        list[listed] = n;
-        lrow[listed] = dev;
-        a.free_top[inst] = max(0, idx);
-        a.n_out[inst] = n_out;
-        a.n_in[inst] = restored;
-        a.n_active[inst] = listed + 1;
-        atomicAdd(a.listed_total, (unsigned long long)(listed + 1));
-        if (n_out) atomicAdd(a.xfer + 0, (unsigned long long)n_out);
-        if (restored) atomicAdd(a.xfer + 1, (unsigned long long)restored);
-        if (pushed) atomicAdd(a.xfer + 2, (unsigned long long)pushed);
-    }
+    if (tid == 0) spill_tail(a, inst, base, n, listed, need, popped, n_out, released, back);
 }
 
-// Spill mode for few, long instances: the same two passes cut into segments,
-// as three launches (pass 1 must push every released row before pass 2 pops).
-//   S1  recovery, then per segment: released rows, rows to copy out, positions
-//       that need a row back, listed positions;
-//   S2  releases (pushes in position order after the counts of the segments
-//       before), out-list entries;
-//   S3  the list and the rows it needs (pops in position order), and the tail.
+// Spill mode for few, long instances: the same passes cut into segments of
+// seg_len positions, as four launches:
+//   S1  the freeze loop and recovery; per segment: positions listed
+//   S2  releases, out-list entries (after the counts of the segments before),
+//       take-backs; per segment: positions that need a row, releases, take-backs
+//   S3  one workgroup per instance: the free rows for the positions that need
+//       one and for the next token
+//   S4  the list and the rows of its entries, and the tail.
 struct SegCounts {
-    int spill, first, need, flag;
+    int first, released, need, listed, back, pad0, pad1, pad2;
 };
 
 // seg_count holds, per instance, n_seg count records and one more whose first
-// field is the stack height at the start of the rebuild (the last segment of
-// S3 overwrites free_top while other segments may still read it).
+// field is the number of free rows found (S3).
+__device__ __forceinline__ SegCounts* seg_records(const CompactArgs& a, int inst) {
+    return reinterpret_cast<SegCounts*>(a.seg_count) + (size_t)inst * (a.n_seg + 1);
+}
+
 __device__ __forceinline__ SegCounts seg_prefix(const CompactArgs& a, int inst, int seg) {
-    const int4* c = reinterpret_cast<const int4*>(a.seg_count) + (size_t)inst * (a.n_seg + 1);
-    SegCounts s{0, 0, 0, 0};
+    const SegCounts* c = seg_records(a, inst);
+    SegCounts s{0, 0, 0, 0, 0, 0, 0, 0};
     for (int k = 0; k < seg; ++k) {
-        const int4 v = c[k];
-        s.spill += v.x; s.first += v.y; s.need += v.z; s.flag += v.w;
+        s.first += c[k].first; s.released += c[k].released; s.need += c[k].need;
+        s.listed += c[k].listed; s.back += c[k].back;
     }
     return s;
 }
@@ -493,51 +605,45 @@ spill_count_kernel(CompactArgs a) {
     const Ladder r = make_ladder(a, b, n);
     const size_t base = (size_t)inst * a.cap;
     int32_t* U = a.unfreeze + base;
-    const int32_t* row_of = a.row_of + base;
-    const uint8_t* on_host = a.on_host + base;
-    int ns = 0, nf = 0, nn = 0, nl = 0;
+    int nl = 0, nf = 0;
     for (int p0 = lo; p0 < hi; p0 += 4 * kThreads) {
         const int p = p0 + 4 * threadIdx.x;
         Tile4 cur;
         load_tile(a, base, p, hi, cur);
         int (&u)[4] = cur.u;
         int row[4];
-        load4(row_of, p, hi, row, -1);
-        bool spill[4], first[4], need[4], flag[4];
+        load4(a.row_of + base, p, hi, row, -1);
         bool dirty = freeze4(a, base, p, hi, n, u, cur.c, cur.f);
+        bool listed[4], first[4];
 #pragma unroll
         for (int k = 0; k < 4; ++k) {
             bool hit;
             const bool live = p + k < hi;
             u[k] = recover(r, u[k], p + k, live, hit);
             dirty |= hit;
-            spill[k] = live & (row[k] >= 0) & (u[k] > r.t1) & (u[k] - a.t >= a.spill_min_D);
-            const bool stored = live ? on_host[p + k] != 0 : true;
-            first[k] = spill[k] & !stored;
-            flag[k] = live & (u[k] <= r.t1);
-            need[k] = flag[k] & (row[k] < 0);
+            listed[k] = live & (u[k] <= r.t1);
+            const bool rel = live & (row[k] >= 0) & (u[k] > r.t1) & (u[k] - a.t >= a.spill_min_D);
+            first[k] = rel & (live ? a.on_host[base + p + k] == 0 : false);
         }
         if (dirty) {
             for (int k = 0; k < 4; ++k) if (p + k < hi) U[p + k] = u[k];
         }
         int b0, m0, b1, m1;
-        ballot4(spill, b0, m0);
+        ballot4(listed, b0, m0);
         ballot4(first, b1, m1);
-        const Scan s1 = tile_scan(b0, m0, b1, m1, tot0, tot1);
-        ballot4(need, b0, m0);
-        ballot4(flag, b1, m1);
-        const Scan s2 = tile_scan(b0, m0, b1, m1, tot0, tot1);
-        ns += s1.tot0; nf += s1.tot1; nn += s2.tot0; nl += s2.tot1;
+        const Scan sc = tile_scan(b0, m0, b1, m1, tot0, tot1);
+        nl += sc.tot0;
+        nf += sc.tot1;
     }
     if (threadIdx.x == 0) {
-        int4* rec = reinterpret_cast<int4*>(a.seg_count) + (size_t)inst * (a.n_seg + 1);
-        rec[seg] = make_int4(ns, nf, nn, nl);
-        if (seg == 0) rec[a.n_seg] = make_int4(a.free_top[inst], 0, 0, 0);
+        SegCounts* rec = seg_records(a, inst);
+        rec[seg].listed = nl;
+        rec[seg].first = nf;
     }
 }
 
 __global__ void __launch_bounds__(kThreads)
-spill_push_kernel(CompactArgs a) {
+spill_release_kernel(CompactArgs a) {
     __shared__ int tot0[kWaves], tot1[kWaves];
     __shared__ SegCounts pre;
     const int seg = blockIdx.x, inst = blockIdx.y;
@@ -545,58 +651,64 @@ spill_push_kernel(CompactArgs a) {
     const int n = begin_rebuild(a, b, false);
     if (n < 0) return;
     const int lo = seg * a.seg_len, hi = min(n, lo + a.seg_len);
-    if (lo >= hi) return;
     if (threadIdx.x == 0) pre = seg_prefix(a, inst, seg);
     __syncthreads();
     const Ladder r = make_ladder(a, b, n);
     const size_t base = (size_t)inst * a.cap;
-    const int32_t* U = a.unfreeze + base;
-    int32_t* row_of = a.row_of + base;
-    uint8_t* on_host = a.on_host + base;
-    int32_t* stack = a.free_rows + (size_t)inst * a.pool_rows;
-    const int top0 = reinterpret_cast<const int4*>(a.seg_count)[(size_t)inst * (a.n_seg + 1) + a.n_seg].x;
-    int pushed = pre.spill, n_out = pre.first;
+    int n_out = pre.first, nr = 0, nn = 0, nb = 0;
     for (int p0 = lo; p0 < hi; p0 += 4 * kThreads) {
         const int p = p0 + 4 * threadIdx.x;
-        int u[4], row[4];
-        load4(U, p, hi, u, 0);                // already recovered by S1
-        load4(row_of, p, hi, row, -1);
-        bool spill[4], first[4];
-#pragma unroll
-        for (int k = 0; k < 4; ++k) {
-            const bool live = p + k < hi;
-            spill[k] = live & (row[k] >= 0) & (u[k] > r.t1) & (u[k] - a.t >= a.spill_min_D);
-            const bool stored = live ? on_host[p + k] != 0 : true;
-            first[k] = spill[k] & !stored;
-        }
+        int u[4];
+        load4(a.unfreeze + base, p, hi, u, 0);      // already updated by S1
+        SpillFlags f;
+        spill_decide(a, r, base, p, hi, u, f);
         int b0, m0, b1, m1;
-        ballot4(spill, b0, m0);
-        ballot4(first, b1, m1);
-        const Scan sc = tile_scan(b0, m0, b1, m1, tot0, tot1);
-        int ps = top0 + pushed + sc.off0, po = n_out + sc.off1;
+        ballot4(f.first, b0, m0);
+        ballot4(f.released, b1, m1);
+        const Scan s1 = tile_scan(b0, m0, b1, m1, tot0, tot1);
+        int po = n_out + s1.off0;
 #pragma unroll
         for (int k = 0; k < 4; ++k) {
-            if (first[k]) {
-                a.out_pos[base + po] = p + k;
-                a.out_row[base + po] = row[k];
-                on_host[p + k] = 1;
-                ++po;
-            }
-            if (spill[k]) {
-                if (ps < a.pool_rows) stack[ps] = row[k];
-                row_of[p + k] = -1;
-                ++ps;
-            }
+            if (!f.first[k]) continue;
+            a.out_pos[base + po] = p + k;
+            a.out_row[base + po] = a.last_row[base + p + k];
+            ++po;
         }
-        pushed += sc.tot0;
-        n_out += sc.tot1;
+        ballot4(f.need, b0, m0);
+        ballot4(f.back, b1, m1);
+        const Scan s2 = tile_scan(b0, m0, b1, m1, tot0, tot1);
+        n_out += s1.tot0;
+        nr += s1.tot1;
+        nn += s2.tot0;
+        nb += s2.tot1;
     }
+    if (threadIdx.x == 0) {
+        SegCounts* rec = seg_records(a, inst);
+        rec[seg].released = nr;
+        rec[seg].need = nn;
+        rec[seg].back = nb;
+    }
+}
+
+__global__ void __launch_bounds__(kThreads)
+spill_rows_kernel(CompactArgs a) {
+    __shared__ int tot0[kWaves], tot1[kWaves];
+    __shared__ int last_idx, need;
+    const int inst = blockIdx.x;
+    const int b = inst % a.B;
+    const int n = begin_rebuild(a, b, false);
+    if (n < 0) return;
+    if (threadIdx.x == 0) need = seg_prefix(a, inst, a.n_seg).need;
+    __syncthreads();
+    const int popped = find_free_rows(a, inst, need + 1, tot0, tot1, &last_idx);
+    if (threadIdx.x == 0) seg_records(a, inst)[a.n_seg].first = popped;
 }
 
 __global__ void __launch_bounds__(kThreads)
 spill_list_kernel(CompactArgs a) {
     __shared__ int tot0[kWaves], tot1[kWaves];
     __shared__ SegCounts pre, all;
+    __shared__ int popped;
     const int seg = blockIdx.x, inst = blockIdx.y;
     const int b = inst % a.B;
     const int n = begin_rebuild(a, b, false);
@@ -607,79 +719,36 @@ spill_list_kernel(CompactArgs a) {
     if (threadIdx.x == 0) {
         pre = seg_prefix(a, inst, seg);
         all = seg_prefix(a, inst, a.n_seg);
+        popped = seg_records(a, inst)[a.n_seg].first;
     }
     __syncthreads();
     const Ladder r = make_ladder(a, b, n);
     const size_t base = (size_t)inst * a.cap;
-    const int32_t* U = a.unfreeze + base;
-    int32_t* row_of = a.row_of + base;
-    const int32_t* stack = a.free_rows + (size_t)inst * a.pool_rows;
-    const int top0 = reinterpret_cast<const int4*>(a.seg_count)[(size_t)inst * (a.n_seg + 1) + a.n_seg].x;
-    const int top = min(a.pool_rows, top0 + all.spill);
-    int listed = pre.flag, popped = pre.need;
+    int listed = pre.listed, pn_run = pre.need;
     bool short_of_rows = false;
     for (int p0 = lo; p0 < hi; p0 += 4 * kThreads) {
         const int p = p0 + 4 * threadIdx.x;
         int u[4], row[4];
-        load4(U, p, hi, u, 0);
-        load4(row_of, p, hi, row, -1);
-        bool flag[4], need[4];
+        load4(a.unfreeze + base, p, hi, u, 0);
+        load4(a.row_of + base, p, hi, row, -1);
+        SpillFlags f;
 #pragma unroll
         for (int k = 0; k < 4; ++k) {
-            flag[k] = (p + k < hi) & (u[k] <= r.t1);
-            need[k] = flag[k] & (row[k] < 0);
+            f.listed[k] = (p + k < hi) & (u[k] <= r.t1);
+            f.need[k] = f.listed[k] & (row[k] < 0);
+            f.row[k] = row[k];
         }
         int b0, m0, b1, m1;
-        ballot4(flag, b0, m0);
-        ballot4(need, b1, m1);
+        ballot4(f.listed, b0, m0);
+        ballot4(f.need, b1, m1);
         const Scan sc = tile_scan(b0, m0, b1, m1, tot0, tot1);
-        int pl = listed + sc.off0, pn = popped + sc.off1;
-#pragma unroll
-        for (int k = 0; k < 4; ++k) {
-            if (!flag[k]) continue;
-            int dev = row[k];
-            if (need[k]) {
-                const int idx = top - 1 - pn;
-                if (idx >= 0) {
-                    dev = stack[idx];
-                    row_of[p + k] = dev;
-                    a.in_pos[base + pn] = p + k;
-                    a.in_row[base + pn] = dev;
-                } else {
-                    dev = 0;                  // no row left: results are void, the host is told
-                    short_of_rows = true;
-                }
-                ++pn;
-            }
-            a.list[base + pl] = p + k;
-            a.list_row[base + pl] = dev;
-            ++pl;
-        }
+        spill_list4(a, base, inst, p, f, listed + sc.off0, pn_run + sc.off1, popped, short_of_rows);
         listed += sc.tot0;
-        popped += sc.tot1;
+        pn_run += sc.tot1;
     }
     if (short_of_rows) a.flags[0] = 1;
-    if (seg == last && threadIdx.x == 0) {
-        const int idx = top - 1 - all.need;   // the next token's row
-        int dev = 0;
-        if (idx >= 0) {
-            dev = stack[idx];
-            row_of[n] = dev;
-        } else {
-            a.flags[0] = 1;
-        }
-        a.list[base + all.flag] = n;
-        a.list_row[base + all.flag] = dev;
-        a.free_top[inst] = max(0, idx);
-        const int restored = min(all.need, top);
-        a.n_out[inst] = all.first;
-        a.n_in[inst] = restored;
-        a.n_active[inst] = all.flag + 1;
-        atomicAdd(a.listed_total, (unsigned long long)(all.flag + 1));
-        if (all.first) atomicAdd(a.xfer + 0, (unsigned long long)all.first);
-        if (restored) atomicAdd(a.xfer + 1, (unsigned long long)restored);
-        if (all.spill) atomicAdd(a.xfer + 2, (unsigned long long)all.spill);
-    }
+    if (seg == last && threadIdx.x == 0)
+        spill_tail(a, inst, base, n, all.listed, all.need, popped, all.first, all.released, all.back);
 }
 
 __global__ void __launch_bounds__(256)
@@ -689,12 +758,12 @@ spill_init_kernel(SpillInitArgs a) {
     const size_t base = (size_t)inst * a.cap;
     for (int p = threadIdx.x; p < a.cap; p += blockDim.x) {
         a.row_of[base + p] = p < P ? p : -1;
+        a.last_row[base + p] = -1;
         a.on_host[base + p] = 0;
     }
-    const int free_n = max(0, a.pool_rows - P);
-    int32_t* stack = a.free_rows + (size_t)inst * a.pool_rows;
-    for (int k = threadIdx.x; k < free_n; k += blockDim.x) stack[k] = a.pool_rows - 1 - k;
-    if (threadIdx.x == 0) a.free_top[inst] = free_n;
+    int32_t* owner = a.row_owner + (size_t)inst * a.pool_rows;
+    for (int r = threadIdx.x; r < a.pool_rows; r += blockDim.x) owner[r] = r < P ? r : -1;
+    if (threadIdx.x == 0) a.hand[inst] = a.pool_rows > P ? P : 0;
 }
 
 }  // namespace
@@ -705,7 +774,10 @@ hipError_t launch_compact(const CompactArgs& a, int n_instances, hipStream_t s) 
         hipLaunchKernelGGL(spill_count_kernel, grid, dim3(kThreads), 0, s, a);
         hipError_t e = hipGetLastError();
         if (e != hipSuccess) return e;
-        hipLaunchKernelGGL(spill_push_kernel, grid, dim3(kThreads), 0, s, a);
+        hipLaunchKernelGGL(spill_release_kernel, grid, dim3(kThreads), 0, s, a);
+        e = hipGetLastError();
+        if (e != hipSuccess) return e;
+        hipLaunchKernelGGL(spill_rows_kernel, dim3(n_instances), dim3(kThreads), 0, s, a);
         e = hipGetLastError();
         if (e != hipSuccess) return e;
         hipLaunchKernelGGL(spill_list_kernel, grid, dim3(kThreads), 0, s, a);

@@ -123,15 +123,18 @@ struct CompactArgs {
     int32_t* row_of;          // [L][B][cap] device row of a position, -1: host store only
     uint8_t* on_host;         // [L][B][cap] 1: the host store holds the position's rows
     int32_t* list_row;        // [L][B][cap] device row of each listed position
-    int32_t* free_rows;       // [L][B][pool_rows] stack of free device rows
-    int32_t* free_top;        // [L][B] stack height
+    int32_t* last_row;        // [L][B][cap] the device row a host-only position held last
+    int32_t* row_owner;       // [L][B][pool_rows] position whose K/V a row holds, -1: none
+    int32_t* hand;            // [L][B] where the next search for free rows starts
+    int32_t* pop_buf;         // [L][B][pool_rows] the free rows found for this rebuild
     int32_t* out_pos;         // [L][B][cap] rows to copy to the host store: position ...
     int32_t* out_row;         //   ... and the device row it leaves
     int32_t* n_out;           // [L][B]
     int32_t* in_pos;          // [L][B][cap] rows to copy back: position ...
     int32_t* in_row;          //   ... and the device row it takes
     int32_t* n_in;            // [L][B]
-    unsigned long long* xfer; // [0] rows to host, [1] rows from host, [2] device rows released
+    unsigned long long* xfer; // [0] rows to host, [1] rows from host, [2] device rows released,
+                              // [3] rows taken back intact (no copy)
     // the freeze loop of step t runs here, before recovery (not before step 1)
     int32_t freeze;           // 1: apply the step's freeze loop (set on the device: t > 0)
     const uint8_t* flag;      // [L][B][cap] layer scope: 1 where the position scored below tau at step t
@@ -150,12 +153,14 @@ struct CompactArgs {
 };
 
 // First decode step in spill mode: prompt positions p < P sit in device rows
-// p, the other rows are free (lowest handed out first), nothing is on the host.
+// p, the other rows are free (the search for free rows starts at row P),
+// nothing is on the host.
 struct SpillInitArgs {
     int32_t* row_of;
     uint8_t* on_host;
-    int32_t* free_rows;
-    int32_t* free_top;
+    int32_t* last_row;
+    int32_t* row_owner;
+    int32_t* hand;
     const int32_t* plen;
     int32_t B, cap, pool_rows;
 };

@@ -137,8 +137,10 @@ struct asrkf_ctx {
     int32_t* row_of = nullptr;
     uint8_t* on_host = nullptr;
     int32_t* list_row = nullptr;
-    int32_t* free_rows = nullptr;
-    int32_t* free_top = nullptr;
+    int32_t* last_row = nullptr;  // [L][B][cap] row a host-only position held last
+    int32_t* row_owner = nullptr; // [L][B][pool_rows] position whose K/V a row holds
+    int32_t* hand = nullptr;      // [L][B] start of the next free-row search
+    int32_t* pop_buf = nullptr;   // [L][B][pool_rows] free rows found by a rebuild
     int32_t* out_pos = nullptr;
     int32_t* out_row = nullptr;
     int32_t* n_out = nullptr;
@@ -222,8 +224,8 @@ void free_all(asrkf_ctx* ctx) {
     void* ptrs[] = {ctx->kpool, ctx->vpool, ctx->unfreeze, ctx->count, ctx->flag, ctx->list,
                     ctx->n_active, ctx->plen, ctx->dur, ctx->escalation, ctx->level,
                     ctx->entropy, ctx->pmax, ctx->part_acc, ctx->part_ml, ctx->slot_info, ctx->ent_partial, ctx->ent_ticket,
-                    ctx->counters, ctx->row_of, ctx->on_host, ctx->list_row, ctx->free_rows,
-                    ctx->free_top, ctx->out_pos, ctx->out_row, ctx->n_out, ctx->in_pos, ctx->in_row,
+                    ctx->counters, ctx->row_of, ctx->on_host, ctx->list_row, ctx->last_row,
+                    ctx->row_owner, ctx->hand, ctx->pop_buf, ctx->out_pos, ctx->out_row, ctx->n_out, ctx->in_pos, ctx->in_row,
                     ctx->n_in, ctx->flags, ctx->t_dev, ctx->hmask, ctx->hlast, ctx->rel_acc, ctx->xlog,
                     ctx->norm, ctx->seg_count};
     for (void* p : ptrs) if (p) (void)hipFree(p);
@@ -399,7 +401,7 @@ asrkf_status asrkf_init(const asrkf_config* cfg, asrkf_ctx** out) {
     }
     if (ctx->token_scope) ALLOC(rel_acc, (size_t)c.batch * ctx->cap * 4);
     ctx->n_seg = compact_segments((int)st_inst, ctx->cap, &ctx->seg_len);
-    if (ctx->n_seg > 1) ALLOC(seg_count, st_inst * (ctx->n_seg + 1) * 16);   // spill mode: 4 counts per segment
+    if (ctx->n_seg > 1) ALLOC(seg_count, st_inst * (ctx->n_seg + 1) * 32);   // spill mode: 8 counts per segment
     if (c.relevance == ASRKF_REL_SOFTMAX) {
         ALLOC(xlog, (size_t)c.batch * ctx->cap * c.n_q_heads * 4);
         ALLOC(norm, (size_t)c.batch * c.n_q_heads * 2 * 4);
@@ -423,8 +425,10 @@ asrkf_status asrkf_init(const asrkf_config* cfg, asrkf_ctx** out) {
         ALLOC(row_of, per_pos * 4);
         ALLOC(on_host, per_pos);
         ALLOC(list_row, per_pos * 4);
-        ALLOC(free_rows, inst * ctx->pool_rows * 4);
-        ALLOC(free_top, inst * 4);
+        ALLOC(last_row, per_pos * 4);
+        ALLOC(row_owner, inst * ctx->pool_rows * 4);
+        ALLOC(hand, inst * 4);
+        ALLOC(pop_buf, inst * ctx->pool_rows * 4);
         ALLOC(out_pos, per_pos * 4);
         ALLOC(out_row, per_pos * 4);
         ALLOC(n_out, inst * 4);
@@ -543,8 +547,9 @@ asrkf_status build_lists(asrkf_ctx* ctx, int forced_level, hipStream_t s) {
         SpillInitArgs z{};
         z.row_of = ctx->row_of;
         z.on_host = ctx->on_host;
-        z.free_rows = ctx->free_rows;
-        z.free_top = ctx->free_top;
+        z.last_row = ctx->last_row;
+        z.row_owner = ctx->row_owner;
+        z.hand = ctx->hand;
         z.plen = ctx->plen;
         z.B = ctx->cfg.batch;
         z.cap = ctx->cap;
@@ -589,8 +594,10 @@ asrkf_status build_lists(asrkf_ctx* ctx, int forced_level, hipStream_t s) {
         a.row_of = ctx->row_of;
         a.on_host = ctx->on_host;
         a.list_row = ctx->list_row;
-        a.free_rows = ctx->free_rows;
-        a.free_top = ctx->free_top;
+        a.last_row = ctx->last_row;
+        a.row_owner = ctx->row_owner;
+        a.hand = ctx->hand;
+        a.pop_buf = ctx->pop_buf;
         a.out_pos = ctx->out_pos;
         a.out_row = ctx->out_row;
         a.n_out = ctx->n_out;
@@ -951,6 +958,7 @@ asrkf_status asrkf_stats(asrkf_ctx* ctx, asrkf_stats_t* out) {
     out->rows_to_host = (int64_t)cnt[8];
     out->rows_from_host = (int64_t)cnt[9];
     out->rows_released = (int64_t)cnt[10];
+    out->rows_reused = (int64_t)cnt[11];
     return ASRKF_OK;
 }
 

@@ -143,7 +143,8 @@ def test_recovery_stress_ctx131k():
     finally:
         A.asrkf_destroy(ctx)
     assert glevel == levels
-    print(f"rows to host {stats['rows_to_host']}, restored {stats['rows_from_host']}", flush=True)
+    print(f"rows to host {stats['rows_to_host']}, restored from the host {stats['rows_from_host']}, "
+          f"taken back intact {stats['rows_reused']}", flush=True)
 
     # ---- before the switch: closed-form states, oracle attention over them
     def q_of(t):
@@ -175,4 +176,4 @@ def test_recovery_stress_ctx131k():
             v_star = V[p_star][np.arange(Hq) // w.group]
             assert np.abs(gout[t] - v_star).max() < 0.05
     assert gst[t_s]["res"]["device_row"][p_star] >= 0     # restored from the host store
-    assert stats["rows_from_host"] > 0 and stats["rows_to_host"] > 0
+    assert stats["rows_from_host"] + stats["rows_reused"] > 0 and stats["rows_to_host"] > 0

@@ -5,8 +5,10 @@ outputs within the acceptance bound), plus the residency of every position
 after every step: a position is held only in the host store exactly while it
 is frozen by a freeze of at least spill_min_D steps; the host store holds
 every position that was ever released; resident positions own distinct
-device rows.  Outputs that match the oracle after restores show that the rows
-came back intact from the host store.
+device rows.  Every restore either takes the token's last device row back
+(no other position was written into it since) or copies its rows back from
+the host store; outputs that match the oracle after restores show that the
+rows came back intact either way.
 """
 import math
 
@@ -40,7 +42,7 @@ def _spill_parity(w, inp, modes=None, with_logits=True, side_delay_us=0):
     last = stats[-1]
     released = sum(int(np.count_nonzero(g[k][-1]["on_host"])) for k in instances)
     assert last["rows_to_host"] == released           # each token copied out once
-    assert last["rows_from_host"] == restores
+    assert last["rows_from_host"] + last["rows_reused"] == restores
     print(f"{w.name}: rows to host {last['rows_to_host']}, restores {restores}, "
           f"releases {last['rows_released']}")
     return g, o, mon, stats
@@ -60,8 +62,23 @@ def test_flag_all_spills_and_restores():
     released and restored again and again."""
     w = _flag_all()
     g, o, _, stats = _spill_parity(w, H.Inputs(w))
-    assert stats[-1]["rows_from_host"] > 1000
+    assert stats[-1]["rows_from_host"] + stats[-1]["rows_reused"] > 1000
     assert stats[-1]["rows_released"] > stats[-1]["rows_to_host"]   # rows re-released, not re-copied
+    # a row for every position: only new tokens take free rows, so no released
+    # row is written over and every restore takes its row back without a copy
+    assert stats[-1]["rows_from_host"] == 0
+
+
+def test_flag_all_tight_rows_copy_and_reuse():
+    """The same cohort with just enough device rows: new tokens and restores
+    take rows that released tokens left, so some restores copy from the host
+    store while others still find their rows intact."""
+    w = _flag_all()
+    peak = _resident_peak(w, H.Inputs(w))
+    assert peak < w.max_ctx, peak
+    w = w.replace(device_rows=peak)
+    g, o, _, stats = _spill_parity(w, H.Inputs(w))
+    assert stats[-1]["rows_from_host"] > 0 and stats[-1]["rows_reused"] > 0
 
 
 @pytest.mark.parametrize("shape", [
@@ -72,8 +89,10 @@ def test_flag_all_spill_wide_layouts(shape):
     """Spill mode with the head layouts in which several waves share each token:
     released and restored rows are read through the device-row list."""
     w = _flag_all(name="spill-wide", prefill=[300], steps=40, **shape)
+    w = w.replace(device_rows=_resident_peak(w, H.Inputs(w)))
     g, o, _, stats = _spill_parity(w, H.Inputs(w))
-    assert stats[-1]["rows_from_host"] > 100
+    assert stats[-1]["rows_from_host"] > 0
+    assert stats[-1]["rows_from_host"] + stats[-1]["rows_reused"] > 100
 
 
 def _resident_peak(w, inp):
@@ -133,8 +152,16 @@ def test_restores_wait_for_a_delayed_side_stream():
     import paper_2512_11221_amd as A
     w0 = gen.tiny()
     w = gen.tiny(tau=H.score_quantile(w0, 0.6), spill_min_D=2)
-    inp = H.Inputs(w, H.fix_margin(w))
-    g, o, mon, stats = _spill_parity(w, inp, modes={20: A.SR, 33: A.WR, 47: A.FR},
+    att = H.fix_margin(w)
+    modes = {20: A.SR, 33: A.WR, 47: A.FR}
+    # just enough device rows, so that rows change hands and restores copy
+    o = H.run_oracle(w, H.Inputs(w, att), [(0, 0)], modes, with_logits=False)[(0, 0)]
+    peak = w.prefill[0] + 1
+    for r in o:
+        d = np.array([H.oracle.freeze_duration(int(c), w.k_soft) for c in r["count"]])
+        peak = max(peak, len(r["frozen"]) - int((r["frozen"] & (d >= w.spill_min_D)).sum()) + 1)
+    w = w.replace(device_rows=peak)
+    g, o, mon, stats = _spill_parity(w, H.Inputs(w, att), modes=modes,
                                      with_logits=False, side_delay_us=3000)
     assert stats[-1]["rows_from_host"] > 0
 
@@ -186,6 +213,6 @@ def test_candidates_inside_window_spill():
     w = _flag_all(name="spill-inside", candidates="inside", k_soft=0.5, window_K=48,
                   prefill=[200], steps=48)
     g, o, _, stats = _spill_parity(w, H.Inputs(w))
-    assert stats[-1]["rows_from_host"] > 100
+    assert stats[-1]["rows_from_host"] + stats[-1]["rows_reused"] > 100
     first = [r for r in o[(0, 0)] if r["t"] == 1][0]
     assert first["frozen"][-1]                 # the token appended at step 1 is frozen at once
