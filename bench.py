@@ -9,7 +9,8 @@ HBM before the timed region starts.
 Prints one JSON line.  value = attended (active) KV token-layers per second,
 from a timed loop without instrumentation; the attention kernel's duration for
 the roofline comes from a replay of the same steps in which every attention
-dispatch records HIP events.
+dispatch records HIP events, the per-step series from two more replays (GPU
+time per step from events between steps, attended token-layers per step).
 """
 import argparse
 import json
@@ -144,9 +145,10 @@ def regimes(w, W, K, series, bytes_per_token):
     frozen cohort is out.  A step counts as dense when at least 90 % of the
     positions attend.
     Per regime: attended token-layers per attention launch, the launches'
-    mean duration (the replay's dispatch events), that kernel's fraction of
-    the HBM peak, and the whole step's fraction (algorithmic bytes, the
-    logits included, over the step's GPU time in the replay)."""
+    mean duration (the dispatch events of the kernel replay), that kernel's
+    fraction of the HBM peak, and the whole step's fraction (algorithmic
+    bytes, the logits included, over the step's GPU time from the events
+    between steps)."""
     L, B = w.n_layers, w.batch
     out = {}
     for name in ("dense", "sparse"):
@@ -263,9 +265,19 @@ def main():
     dg.logits(1, S, LG)
     out = torch.empty((L, B, Hq, D), dtype=torch.float32, device="cuda")
 
-    def run_pass(timing):
-        """A fresh context: prompt, W warm-up steps, then K timed steps."""
-        ctx = A.asrkf_init(cfg)
+    ctx = A.asrkf_init(cfg)
+
+    def run_pass(mode):
+        """The context reset (the same device memory in every pass): prompt, W
+        warm-up steps, then K steps measured as `mode` says:
+          rate    no instrumentation; wall clock over the K steps (the value)
+          steps   a HIP event between consecutive steps, no host waits inside
+                  the loop (each step's GPU time)
+          kernel  every attention dispatch records HIP events, no host waits
+                  inside the loop (the kernel's execution time per launch)
+          count   the host reads the counters after every step (attended
+                  token-layers per step; nothing timed)"""
+        A.asrkf_reset(ctx)
         Pmax = max(w.prefill)
         stage_k = torch.empty(Pmax * Hkv * D, dtype=tdt, device="cuda")
         stage_v = torch.empty_like(stage_k)
@@ -286,9 +298,9 @@ def main():
         for t in range(1, W + 1):
             step(t)
         torch.cuda.synchronize()
-        if args.graph and not timing:
-            # every timed step captured beforehand as its own HIP graph (the same kernels,
-            # reading that step's inputs); the timed loop launches the graphs in order
+        if args.graph and mode in ("rate", "steps"):
+            # every measured step captured beforehand as its own HIP graph (the same
+            # kernels, reading that step's inputs); the loop launches the graphs in order
             graphs = []
             for t in range(W + 1, W + K + 1):
                 g = torch.cuda.CUDAGraph()
@@ -300,42 +312,49 @@ def main():
             def step(t):                                         # noqa: F811
                 graphs[t - W - 1].replay()
         A.asrkf_stats_reset(ctx)
-        A.asrkf_set_timing(ctx, timing)
+        A.asrkf_set_timing(ctx, mode == "kernel")
+        marks = [torch.cuda.Event(enable_timing=True) for _ in range(K + 1)] if mode == "steps" else []
+        attended = []
         torch.cuda.synchronize()
-        series = {"gpu_ms": [], "attended": [], "attn_ms": []}
         t0 = time.perf_counter()
+        if marks:
+            marks[0].record()
         for t in range(W + 1, W + K + 1):
-            if timing:
-                # the replay also records the per-step series: GPU time and attended
-                # token-layers of every step (the freezing cohort moves in lockstep)
-                e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-                e0.record()
-                step(t)
-                e1.record()
-                e1.synchronize()
-                series["gpu_ms"].append(round(e0.elapsed_time(e1), 4))
-                st_t = A.asrkf_stats(ctx)
-                series["attended"].append(st_t["attended_total"])
-                series["attn_ms"].append(st_t["attn_kernel_ms"])
-            else:
-                step(t)
+            step(t)
+            if marks:
+                marks[t - W].record()
+            elif mode == "count":
+                attended.append(A.asrkf_stats(ctx)["attended_total"])
         torch.cuda.synchronize()
         elapsed = time.perf_counter() - t0
         st = A.asrkf_stats(ctx)
-        A.asrkf_destroy(ctx)
-        if timing:
-            for key in ("attended", "attn_ms"):
-                cum = series[key]
-                series[key] = [c - p for c, p in zip(cum, [0] + cum[:-1])]
-            series["attn_ms"] = [round(x, 5) for x in series["attn_ms"]]
+        series = {}
+        if mode == "steps":
+            series["gpu_ms"] = [round(a.elapsed_time(b), 4) for a, b in zip(marks[:-1], marks[1:])]
+        elif mode == "kernel":
+            ms = A.asrkf_timing_series(ctx)
+            assert len(ms) == K * L, (len(ms), K * L)
+            series["launch_ms"] = [float(x) for x in ms]
+            series["attn_ms"] = [round(float(ms[i * L:(i + 1) * L].sum()), 5) for i in range(K)]
+        elif mode == "count":
+            series["attended"] = [c - p for c, p in zip(attended, [0] + attended[:-1])]
         return elapsed, st, series
 
-    # The step rate comes from a pass without instrumentation; the attention
-    # kernel's duration from a replay of the same steps in which every
-    # attention dispatch records HIP events (those add a few us per launch).
-    elapsed, st, _ = run_pass(False)
-    _, st_timed, series = run_pass(True)
-    assert st_timed["attended_total"] == st["attended_total"]
+    # The step rate comes from a pass without instrumentation.  The same steps
+    # are then replayed three more times on the same context (reset in between,
+    # so every pass reads and writes the same device memory): with a HIP event between steps (each
+    # step's GPU time), with HIP events recorded by every attention dispatch
+    # (the kernel's execution time per launch, for the roofline), and with the
+    # counters read after every step (attended token-layers per step).  None of
+    # the measured passes waits on the host inside its loop.
+    elapsed, st, _ = run_pass("rate")
+    _, _, s_steps = run_pass("steps")
+    _, st_timed, s_kernel = run_pass("kernel")
+    _, st_count, s_count = run_pass("count")
+    assert st_timed["attended_total"] == st["attended_total"] == st_count["attended_total"]
+    assert sum(s_count["attended"]) == st["attended_total"]
+    A.asrkf_destroy(ctx)
+    series = {"gpu_ms": s_steps["gpu_ms"], "attended": s_count["attended"], "attn_ms": s_kernel["attn_ms"]}
     del Q, Kn, Vn, LG, out
 
     attended = st["attended_total"]
@@ -395,7 +414,8 @@ def main():
                      "algorithmic_bytes_per_launch": bytes_per_token * attended
                      / max(1, st_timed["attn_launches"]),
                      "timing": "HIP events recorded by each attention dispatch, in a replay "
-                               "of the same warm-up and timed steps"},
+                               "of the same warm-up and measured steps with no host waits "
+                               "inside the loop"},
     }
     line["roofline"].update(regimes(w, W, K, series, bytes_per_token))
     line["metadata"] = metadata_bytes(w, W, K, attended, algo_bytes, traffic, line["roofline"])

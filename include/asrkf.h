@@ -225,6 +225,15 @@ asrkf_status asrkf_stats_reset(asrkf_ctx* ctx);
  * execution time.  Host-side switch. */
 asrkf_status asrkf_set_timing(asrkf_ctx* ctx, int32_t enable);
 
+/* The execution time of every timed attention launch since the last
+ * asrkf_stats_reset, in launch order (milliseconds).
+ *   ms:    host, room for cap values (may be NULL when cap = 0)
+ *   count: receives the number of timed launches; min(cap, *count) values
+ *          are written.
+ * EINVAL for a null count or a negative cap.  Waits for all queued work of
+ * the context. */
+asrkf_status asrkf_timing_series(asrkf_ctx* ctx, float* ms, int64_t cap, int64_t* count);
+
 /* Token states of one (layer, sequence) after the last completed step t
  * (test export; with ASRKF_SCOPE_TOKEN every layer shows the sequence's one
  * state).  All outputs are host buffers of at least max_ctx entries
@@ -270,6 +279,13 @@ asrkf_status asrkf_get_seq(asrkf_ctx* ctx, int32_t seq, float* entropy, float* p
  * exact for the float32 value k_soft (the table the library uses).
  * out: host, n entries.  EINVAL if k_soft is outside [2^-8, 2^16] or n < 1. */
 asrkf_status asrkf_schedule_table(float k_soft, int32_t n, int32_t* out);
+
+/* Return the context to the state asrkf_init leaves it in (no prompts, no
+ * step, counters and timing cleared, timing off) and keep every allocation,
+ * so that the next batch of sequences reuses the same device memory: prefill
+ * follows as after asrkf_init.  ESTATE while the context's last stream is
+ * being captured.  Waits for all queued work of the context. */
+asrkf_status asrkf_reset(asrkf_ctx* ctx);
 
 /* Free everything the context owns.  Waits for its queued work.  NULL is a no-op. */
 void asrkf_destroy(asrkf_ctx* ctx);

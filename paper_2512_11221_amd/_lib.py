@@ -83,6 +83,8 @@ def load():
         "asrkf_stats": ([P, ctypes.POINTER(asrkf_stats_t)], I32),
         "asrkf_stats_reset": ([P], I32),
         "asrkf_set_timing": ([P, I32], I32),
+        "asrkf_timing_series": ([P, P, ctypes.c_int64, P], I32),
+        "asrkf_reset": ([P], I32),
         "asrkf_debug_delay_side": ([P, I32], I32),
         "asrkf_get_state": ([P, I32, I32, P, P, P, P, P, P], I32),
         "asrkf_get_seq": ([P, I32, P, P, P, P], I32),
@@ -189,6 +191,21 @@ def asrkf_debug_delay_side(ctx, microseconds):
 
 def asrkf_set_timing(ctx, enable):
     _check(load().asrkf_set_timing(ctx, 1 if enable else 0))
+
+
+def asrkf_reset(ctx):
+    _check(load().asrkf_reset(ctx))
+
+
+def asrkf_timing_series(ctx):
+    """Execution times (ms) of the timed attention launches since the last
+    stats reset, in launch order, as a numpy float32 array."""
+    import numpy as np
+    n = ctypes.c_int64()
+    _check(load().asrkf_timing_series(ctx, None, 0, ctypes.byref(n)))
+    ms = np.zeros(max(1, n.value), np.float32)
+    _check(load().asrkf_timing_series(ctx, ms.ctypes.data, n.value, ctypes.byref(n)))
+    return ms[:n.value]
 
 
 def asrkf_get_state(ctx, layer, seq, max_ctx):

@@ -46,6 +46,7 @@ namespace {
 
 constexpr int kThreads = 1024;
 constexpr int kWaves = kThreads / 64;
+constexpr int kDurLds = 1024;                 // Eq. 3 durations cached in LDS
 
 __device__ __forceinline__ int lanes_below(unsigned long long mask) {
     return __builtin_amdgcn_mbcnt_hi((unsigned)(mask >> 32),
@@ -78,8 +79,9 @@ __device__ __forceinline__ Ladder make_ladder(const CompactArgs& a, int b, int n
 // each, layer scope).  With a cumulative count (history_W = 0) the counts come
 // in with U and only changed entries are stored; a finite history window
 // updates the detection bits of a flagged position.  Returns whether u changed.
-__device__ __forceinline__ bool freeze4(const CompactArgs& a, size_t base, int p, int hi, int n,
-                                        int (&u)[4], const int (&cnt)[4], uint32_t flags) {
+__device__ __forceinline__ bool freeze4(const CompactArgs& a, const int32_t* dur_lds, size_t base,
+                                        int p, int hi, int n, int (&u)[4], const int (&cnt)[4],
+                                        uint32_t flags, const float (&rel)[4]) {
     if (!a.freeze) return false;
     bool dirty = false;
     const bool inside = a.cand_inside != 0;
@@ -87,7 +89,7 @@ __device__ __forceinline__ bool freeze4(const CompactArgs& a, size_t base, int p
     for (int k = 0; k < 4; ++k) {
         const int q = p + k;
         bool low;
-        if (a.scope_token) low = q < hi && a.rel_acc[base + q] < a.tau_LH;
+        if (a.scope_token) low = rel[k] < a.tau_LH;
         else low = ((flags >> (8 * k)) & 0xFFu) != 0;
         if (q < hi && u[k] <= a.t && low && freeze_candidate(q, n - a.window_K, inside)) {
             int c;
@@ -97,7 +99,11 @@ __device__ __forceinline__ bool freeze4(const CompactArgs& a, size_t base, int p
             } else {
                 c = detect(a.count, a.hmask, a.hlast, base + q, a.t, a.history_W);
             }
-            const int d = a.dur[min(c, a.dur_len - 1)];
+            // the LDS read is unconditional and the rare global read stays in a
+            // branch of its own (volatile: not merged into a select between the two
+            // addresses, a generic load whose wait also waits for every load in flight)
+            int d = dur_lds[min(c, kDurLds - 1)];
+            if (c >= kDurLds) d = *reinterpret_cast<const volatile int32_t*>(a.dur + min(c, a.dur_len - 1));
             if (d >= 1) {
                 u[k] = a.t + d;
                 dirty = true;
@@ -107,25 +113,55 @@ __device__ __forceinline__ bool freeze4(const CompactArgs& a, size_t base, int p
     return dirty;
 }
 
-// U, counts and flags of the 4 positions p .. p+3 (those below hi), as the
-// freeze loop reads them; counts and flags only when the step freezes.
+// Eq. 3 durations of the counts below kDurLds, staged in LDS by every
+// workgroup that runs the freeze loop (one load per thread, before its tiles).
+__device__ __forceinline__ void load_durations(const CompactArgs& a, int32_t* dur_lds) {
+    if (!a.freeze) return;                    // uniform over the workgroup
+    for (int c = threadIdx.x; c < kDurLds; c += kThreads) dur_lds[c] = a.dur[min(c, a.dur_len - 1)];
+    __syncthreads();
+}
+
+// U, counts and flags of the 4 positions p .. p+3, loaded as they are: the
+// entries at or past the range end hold whatever the rows hold there, and
+// every use checks the position first.  Counts and flags are loaded in every
+// mode (the arrays always exist), so the loads sit in straight-line code:
+// a load inside a branch makes the compiler wait for it, and for everything
+// in flight before it, before the branches join.  State rows hold cap
+// entries, a multiple of 64, and start 16-byte aligned, so the load at
+// min(p, cap - 4) stays inside the row for any p.
 struct Tile4 {
     int u[4], c[4];
     uint32_t f;
+    float r[4];                               // token scope: relevance summed over layers
 };
 
-__device__ __forceinline__ void load_tile(const CompactArgs& a, size_t base, int p, int hi, Tile4& x) {
-    load4(a.unfreeze + base, p, hi, x.u, 0);
-    x.f = 0;
-    if (a.freeze) {
-        if (a.history_W == 0) load4(a.count + base, p, hi, x.c, 0);
-        if (!a.scope_token) {
-            if (p + 3 < hi) {
-                x.f = *reinterpret_cast<const uint32_t*>(a.flag + base + p);
-            } else {
+__device__ __forceinline__ void load_tile(const CompactArgs& a, size_t base, int p, Tile4& x) {
+    const size_t q = base + (size_t)min(p, a.cap - 4);
+    const int4 u = *reinterpret_cast<const int4*>(a.unfreeze + q);
+    const int4 c = *reinterpret_cast<const int4*>(a.count + q);
+    x.f = *reinterpret_cast<const uint32_t*>(a.flag + q);
+    if (a.scope_token) {                      // uniform; the sums exist in token scope only
+        const float4 r = *reinterpret_cast<const float4*>(a.rel_acc + q);
+        x.r[0] = r.x; x.r[1] = r.y; x.r[2] = r.z; x.r[3] = r.w;
+    }
+    x.u[0] = u.x; x.u[1] = u.y; x.u[2] = u.z; x.u[3] = u.w;
+    x.c[0] = c.x; x.c[1] = c.y; x.c[2] = c.z; x.c[3] = c.w;
+}
+
+__device__ __forceinline__ void load_u(const int32_t* U, int p, int cap, int (&u)[4]) {
+    const int4 x = *reinterpret_cast<const int4*>(U + min(p, cap - 4));
+    u[0] = x.x; u[1] = x.y; u[2] = x.z; u[3] = x.w;
+}
+
+// The entries of a loaded tile at or past hi set to their neutral values
+// (U 0, count 0, flag 0), for code that reads them without checking.
+__device__ __forceinline__ void mask_tile(Tile4& x, int p, int hi) {
 #pragma unroll
-                for (int k = 0; k < 4; ++k) x.f |= (p + k < hi ? (uint32_t)a.flag[base + p + k] : 0u) << (8 * k);
-            }
+    for (int k = 0; k < 4; ++k) {
+        if (p + k >= hi) {
+            x.u[k] = 0;
+            x.c[k] = 0;
+            x.f &= ~(0xFFu << (8 * k));
         }
     }
 }
@@ -201,29 +237,30 @@ __device__ __forceinline__ void ballot4(const bool (&f)[4], int& before, int& mi
 // The rebuild of positions [lo, hi) of one instance.  MODE 0 applies the
 // step's updates (freeze loop, recovery) and writes the list;
 // MODE 1 applies the updates and only counts; MODE 2 writes the list from
-// the already updated U.  List entries start at list + out_base.  Returns
-// the number of listed positions (the same value in every thread).
+// the already updated U.  List entries start at list + out_base.  The next
+// tile's loads are in flight while a tile is processed.  Returns the number
+// of listed positions (the same value in every thread).
 template <int MODE>
-__device__ int compact_range(const CompactArgs& a, const Ladder& r, size_t base, int n, int lo,
-                             int hi, int out_base, int* tot0, int* tot1) {
+__device__ int compact_range(const CompactArgs& a, const Ladder& r, const int32_t* dur_lds, size_t base,
+                             int n, int lo, int hi, int out_base, int* tot0, int* tot1) {
     int32_t* U = a.unfreeze + base;
     int32_t* list = a.list + base;
     const int tid = threadIdx.x;
     int listed = 0;
     Tile4 next;
-    if constexpr (MODE != 2) load_tile(a, base, lo + 4 * tid, hi, next);
-    else load4(U, lo + 4 * tid, hi, next.u, 0);
+    if constexpr (MODE != 2) load_tile(a, base, lo + 4 * tid, next);
+    else load_u(U, lo + 4 * tid, a.cap, next.u);
     for (int p0 = lo; p0 < hi; p0 += 4 * kThreads) {
         const int p = p0 + 4 * tid;
         Tile4 cur = next;
         int (&u)[4] = cur.u;
         if (p0 + 4 * kThreads < hi) {                                            // next tile in flight
-            if constexpr (MODE != 2) load_tile(a, base, p + 4 * kThreads, hi, next);
-            else load4(U, p + 4 * kThreads, hi, next.u, 0);
+            if constexpr (MODE != 2) load_tile(a, base, p + 4 * kThreads, next);
+            else load_u(U, p + 4 * kThreads, a.cap, next.u);
         }
         bool flag[4];
         if constexpr (MODE != 2) {
-            bool dirty = freeze4(a, base, p, hi, n, u, cur.c, cur.f);
+            bool dirty = freeze4(a, dur_lds, base, p, hi, n, u, cur.c, cur.f, cur.r);
 #pragma unroll
             for (int k = 0; k < 4; ++k) {
                 bool hit;
@@ -233,7 +270,8 @@ __device__ int compact_range(const CompactArgs& a, const Ladder& r, size_t base,
                 flag[k] = live & (u[k] <= r.t1);
             }
             if (dirty) {
-                for (int k = 0; k < 4; ++k) if (p + k < hi) U[p + k] = u[k];
+                if (p + 3 < hi) *reinterpret_cast<int4*>(U + p) = make_int4(u[0], u[1], u[2], u[3]);
+                else for (int k = 0; k < 4; ++k) if (p + k < hi) U[p + k] = u[k];
             }
         } else {
 #pragma unroll
@@ -263,13 +301,15 @@ __device__ __forceinline__ void finish_list(const CompactArgs& a, int inst, size
 __global__ void __launch_bounds__(kThreads)
 compact_kernel(CompactArgs a) {
     __shared__ int tot0[kWaves], tot1[kWaves];
+    __shared__ int32_t dur_lds[kDurLds];
     const int inst = blockIdx.x;
     const int b = inst % a.B;
     const int n = begin_rebuild(a, b, true);        // positions after step t
     if (n < 0) return;
     const Ladder r = make_ladder(a, b, n);
     const size_t base = (size_t)inst * a.cap;
-    const int listed = compact_range<0>(a, r, base, n, 0, n, 0, tot0, tot1);
+    load_durations(a, dur_lds);
+    const int listed = compact_range<0>(a, r, dur_lds, base, n, 0, n, 0, tot0, tot1);
     if (threadIdx.x == 0) finish_list(a, inst, base, n, listed);
 }
 
@@ -279,15 +319,17 @@ compact_kernel(CompactArgs a) {
 __global__ void __launch_bounds__(kThreads)
 compact_count_kernel(CompactArgs a) {
     __shared__ int tot0[kWaves], tot1[kWaves];
+    __shared__ int32_t dur_lds[kDurLds];
     const int seg = blockIdx.x, inst = blockIdx.y;
     const int b = inst % a.B;
     const int n = begin_rebuild(a, b, true);
     if (n < 0) return;
+    load_durations(a, dur_lds);
     const int lo = seg * a.seg_len, hi = min(n, lo + a.seg_len);
     int cnt = 0;
     if (lo < hi) {
         const Ladder r = make_ladder(a, b, n);
-        cnt = compact_range<1>(a, r, (size_t)inst * a.cap, n, lo, hi, 0, tot0, tot1);
+        cnt = compact_range<1>(a, r, dur_lds, (size_t)inst * a.cap, n, lo, hi, 0, tot0, tot1);
     }
     if (threadIdx.x == 0) a.seg_count[(size_t)inst * gridDim.x + seg] = cnt;
 }
@@ -313,7 +355,7 @@ compact_write_kernel(CompactArgs a) {
     int cnt = 0;
     if (lo < hi) {
         const Ladder r = make_ladder(a, b, n);
-        cnt = compact_range<2>(a, r, base, n, lo, hi, prefix, tot0, tot1);
+        cnt = compact_range<2>(a, r, nullptr, base, n, lo, hi, prefix, tot0, tot1);
     }
     if (seg == last && threadIdx.x == 0) finish_list(a, inst, base, n, prefix + cnt);
 }
@@ -482,11 +524,13 @@ __global__ void __launch_bounds__(kThreads)
 compact_spill_kernel(CompactArgs a) {
     __shared__ int tot0[kWaves], tot1[kWaves];
     __shared__ int last_idx;
+    __shared__ int32_t dur_lds[kDurLds];
 
     const int inst = blockIdx.x;
     const int b = inst % a.B;
     const int n = begin_rebuild(a, b, true);
     if (n < 0) return;
+    load_durations(a, dur_lds);
     const Ladder r = make_ladder(a, b, n);
     const size_t base = (size_t)inst * a.cap;
     int32_t* U = a.unfreeze + base;
@@ -498,9 +542,10 @@ compact_spill_kernel(CompactArgs a) {
     for (int p0 = 0; p0 < n; p0 += 4 * kThreads) {
         const int p = p0 + 4 * tid;
         Tile4 cur;
-        load_tile(a, base, p, n, cur);
+        load_tile(a, base, p, cur);
+        mask_tile(cur, p, n);
         int (&u)[4] = cur.u;
-        bool dirty = freeze4(a, base, p, n, n, u, cur.c, cur.f);
+        bool dirty = freeze4(a, dur_lds, base, p, n, n, u, cur.c, cur.f, cur.r);
 #pragma unroll
         for (int k = 0; k < 4; ++k) {
             bool hit;
@@ -597,10 +642,12 @@ __device__ __forceinline__ SegCounts seg_prefix(const CompactArgs& a, int inst, 
 __global__ void __launch_bounds__(kThreads)
 spill_count_kernel(CompactArgs a) {
     __shared__ int tot0[kWaves], tot1[kWaves];
+    __shared__ int32_t dur_lds[kDurLds];
     const int seg = blockIdx.x, inst = blockIdx.y;
     const int b = inst % a.B;
     const int n = begin_rebuild(a, b, true);
     if (n < 0) return;
+    load_durations(a, dur_lds);
     const int lo = seg * a.seg_len, hi = min(n, lo + a.seg_len);
     const Ladder r = make_ladder(a, b, n);
     const size_t base = (size_t)inst * a.cap;
@@ -609,11 +656,12 @@ spill_count_kernel(CompactArgs a) {
     for (int p0 = lo; p0 < hi; p0 += 4 * kThreads) {
         const int p = p0 + 4 * threadIdx.x;
         Tile4 cur;
-        load_tile(a, base, p, hi, cur);
+        load_tile(a, base, p, cur);
+        mask_tile(cur, p, hi);
         int (&u)[4] = cur.u;
         int row[4];
         load4(a.row_of + base, p, hi, row, -1);
-        bool dirty = freeze4(a, base, p, hi, n, u, cur.c, cur.f);
+        bool dirty = freeze4(a, dur_lds, base, p, hi, n, u, cur.c, cur.f, cur.r);
         bool listed[4], first[4];
 #pragma unroll
         for (int k = 0; k < 4; ++k) {

@@ -174,6 +174,7 @@ struct asrkf_ctx {
     std::vector<std::pair<hipEvent_t, hipEvent_t>> ev_used, ev_free;
     double attn_ms_done = 0.0;
     int64_t attn_launches = 0;
+    std::vector<float> launch_ms;             // every timed launch, in launch order
     int side_delay_us = 0;              // test hook: side stream waits before its copies
     int device = 0;
     void* static_scratch = nullptr;     // this device's address of the static partials array
@@ -908,6 +909,7 @@ asrkf_status collect_timing(asrkf_ctx* ctx) {
         HIP_OK(ctx, hipEventElapsedTime(&ms, ev.first, ev.second));
         ctx->attn_ms_done += ms;
         ctx->attn_launches += 1;
+        ctx->launch_ms.push_back(ms);
         ctx->ev_free.push_back(ev);
     }
     ctx->ev_used.clear();
@@ -980,6 +982,7 @@ asrkf_status asrkf_stats_reset(asrkf_ctx* ctx) {
     HIP_OK(ctx, hipMemcpy(ctx->counters, cnt, sizeof cnt, hipMemcpyHostToDevice));
     ctx->attn_ms_done = 0.0;
     ctx->attn_launches = 0;
+    ctx->launch_ms.clear();
     return ASRKF_OK;
 }
 
@@ -996,6 +999,20 @@ asrkf_status asrkf_set_timing(asrkf_ctx* ctx, int32_t enable) {
     asrkf_status st = check_ctx(ctx);
     if (st != ASRKF_OK) return st;
     ctx->timing = enable != 0;
+    return ASRKF_OK;
+}
+
+asrkf_status asrkf_timing_series(asrkf_ctx* ctx, float* ms, int64_t cap, int64_t* count) {
+    asrkf_status st = check_ctx(ctx);
+    if (st != ASRKF_OK) return st;
+    if (!count || cap < 0 || (cap > 0 && !ms)) return fail(ASRKF_EINVAL, "bad timing series buffer");
+    st = sync_ctx(ctx);
+    if (st != ASRKF_OK) return st;
+    st = collect_timing(ctx);
+    if (st != ASRKF_OK) return st;
+    const int64_t n = (int64_t)ctx->launch_ms.size();
+    for (int64_t i = 0; i < n && i < cap; ++i) ms[i] = ctx->launch_ms[i];
+    *count = n;
     return ASRKF_OK;
 }
 
@@ -1075,6 +1092,53 @@ asrkf_status asrkf_get_seq(asrkf_ctx* ctx, int32_t seq, float* entropy, float* p
     if (pmax) HIP_OK(ctx, hipMemcpy(pmax, ctx->pmax + seq, 4, hipMemcpyDeviceToHost));
     if (escalation) HIP_OK(ctx, hipMemcpy(escalation, ctx->escalation + seq, 4, hipMemcpyDeviceToHost));
     if (level) HIP_OK(ctx, hipMemcpy(level, ctx->level + seq, 4, hipMemcpyDeviceToHost));
+    return ASRKF_OK;
+}
+
+asrkf_status asrkf_reset(asrkf_ctx* ctx) {
+    asrkf_status st = check_ctx(ctx);
+    if (st != ASRKF_OK) return st;
+    if (ctx->queued && capturing(ctx->last_stream))
+        return fail(ASRKF_ESTATE, "reset while the context's stream is being captured");
+    st = sync_ctx(ctx);
+    if (st != ASRKF_OK) return st;
+    st = collect_timing(ctx);
+    if (st != ASRKF_OK) return st;
+    const asrkf_config& c = ctx->cfg;
+    const size_t st_inst = (size_t)ctx->state_layers * c.batch;
+    const size_t st_pos = st_inst * ctx->cap;
+    // the device state of a context that has run no step: the same values asrkf_init
+    // writes (every other array is written before it is read again), on the stream
+    // of the context's last work, which has just drained
+    hipStream_t s = ctx->last_stream;
+    HIP_OK(ctx, hipMemsetAsync(ctx->unfreeze, 0, st_pos * 4, s));
+    HIP_OK(ctx, hipMemsetAsync(ctx->count, 0, st_pos * 4, s));
+    HIP_OK(ctx, hipMemsetAsync(ctx->n_active, 0, st_inst * 4, s));
+    if (ctx->hmask) HIP_OK(ctx, hipMemsetAsync(ctx->hmask, 0, st_pos * 8, s));
+    if (ctx->hlast) HIP_OK(ctx, hipMemsetAsync(ctx->hlast, 0, st_pos * 4, s));
+    HIP_OK(ctx, hipMemsetAsync(ctx->plen, 0, (size_t)c.batch * 4, s));
+    HIP_OK(ctx, hipMemsetAsync(ctx->escalation, 0, (size_t)c.batch * 4, s));
+    HIP_OK(ctx, hipMemsetAsync(ctx->level, 0, (size_t)c.batch * 4, s));
+    HIP_OK(ctx, hipMemsetAsync(ctx->entropy, 0, (size_t)c.batch * 4, s));
+    HIP_OK(ctx, hipMemsetAsync(ctx->pmax, 0, (size_t)c.batch * 4, s));
+    HIP_OK(ctx, hipMemsetAsync(ctx->ent_ticket, 0, (size_t)c.batch * 4, s));
+    HIP_OK(ctx, hipMemsetAsync(ctx->counters, 0, kCounters * sizeof(unsigned long long), s));
+    HIP_OK(ctx, hipMemsetAsync(ctx->flags, 0, 8, s));
+    HIP_OK(ctx, hipMemsetAsync(ctx->t_dev, 0, 4, s));
+    HIP_OK(ctx, hipStreamSynchronize(s));
+    if (ctx->flags_host) ctx->flags_host[0] = ctx->flags_host[1] = 0;
+    ctx->plen_host.assign(c.batch, 0);
+    ctx->prefilled.assign(c.batch, 0);
+    ctx->t = 0;
+    ctx->next_layer = 0;
+    ctx->lists_ready = false;
+    ctx->xfer_recorded = false;
+    ctx->flag_recorded = false;
+    ctx->timing = false;
+    ctx->attn_ms_done = 0.0;
+    ctx->attn_launches = 0;
+    ctx->launch_ms.clear();
+    ctx->queued = false;
     return ASRKF_OK;
 }
 

@@ -218,12 +218,14 @@ def _dev(x, dtype):
 
 
 def run_gpu(w, inp, instances, modes=None, with_logits=True, steps=None, record=None,
-            timing=False, side_delay_us=0, streams=None):
+            timing=False, side_delay_us=0, streams=None, ctx=None):
     """Run the library; per instance a list of dict(out, unfreeze, count, frozen,
     active_next) for the recorded steps; per sequence the entropy monitor.
     streams(call, t, layer), when given, names the torch stream of each call
     ("prefill", "decode", "restore"; None = the current stream); such a stream
-    first waits for the current stream, where the inputs were copied."""
+    first waits for the current stream, where the inputs were copied.  ctx, when
+    given, is a context of the workload's configuration that has run no step
+    (the caller keeps it); otherwise the run opens and closes its own."""
     import torch
     import paper_2512_11221_amd as A
 
@@ -240,7 +242,9 @@ def run_gpu(w, inp, instances, modes=None, with_logits=True, steps=None, record=
                         wr_last_N=w.wr_last_N, dtype=w.dtype, spill_min_D=w.spill_min_D,
                         device_rows=w.device_rows, history_W=w.history_W,
                         relevance=w.relevance, scope=w.scope, candidates=w.candidates)
-    ctx = A.asrkf_init(cfg)
+    own = ctx is None
+    if own:
+        ctx = A.asrkf_init(cfg)
     if side_delay_us:
         A.asrkf_debug_delay_side(ctx, side_delay_us)
     res = {key: [] for key in instances}
@@ -289,7 +293,8 @@ def run_gpu(w, inp, instances, modes=None, with_logits=True, steps=None, record=
                 stats.append(A.asrkf_stats(ctx))
             del keep
     finally:
-        A.asrkf_destroy(ctx)
+        if own:
+            A.asrkf_destroy(ctx)
     return res, seqmon, stats
 
 

@@ -86,6 +86,8 @@ def test_unknown_option_names_are_refused_by_the_binding():
 def test_null_context_is_einval():
     lib = A.load()
     assert lib.asrkf_set_timing(None, 1) == A._lib.EINVAL
+    assert lib.asrkf_timing_series(None, None, 0, None) == A._lib.EINVAL
+    assert lib.asrkf_reset(None) == A._lib.EINVAL
     assert lib.asrkf_debug_delay_side(None, 5) == A._lib.EINVAL
     assert lib.asrkf_restore(None, None, 0, None) == A._lib.EINVAL
     assert "null context" in A.asrkf_last_error()

@@ -188,3 +188,88 @@ def test_two_contexts_interleaved():
     finally:
         for ctx in ctxs:
             A.asrkf_destroy(ctx)
+
+
+def test_attention_timing_per_launch():
+    """With timing on, every attention launch records its execution time:
+    the series has one positive value per (step, layer), in launch order,
+    sums to the reported total, and a stats reset clears it."""
+    A, ctx = _ctx(L=2, B=2, max_ctx=64)
+    try:
+        q, k, v, out = _io()
+        A.asrkf_decode_step(ctx, 0, q, k, v, out)      # untimed step
+        A.asrkf_decode_step(ctx, 1, q, k, v, out)
+        A.asrkf_restore(ctx, None, A.NONE)
+        A.asrkf_set_timing(ctx, True)
+        for _ in range(3):
+            for l in range(2):
+                A.asrkf_decode_step(ctx, l, q, k, v, out)
+            A.asrkf_restore(ctx, None, A.NONE)
+        ms = A.asrkf_timing_series(ctx)
+        st = A.asrkf_stats(ctx)
+        assert len(ms) == 6 == st["attn_launches"]
+        assert (ms > 0).all() and (ms < 1e3).all()
+        assert abs(float(ms.astype(np.float64).sum()) - st["attn_kernel_ms"]) <= 1e-6 * max(1.0, st["attn_kernel_ms"])
+        A.asrkf_set_timing(ctx, False)
+        A.asrkf_decode_step(ctx, 0, q, k, v, out)
+        A.asrkf_decode_step(ctx, 1, q, k, v, out)
+        A.asrkf_restore(ctx, None, A.NONE)
+        assert len(A.asrkf_timing_series(ctx)) == 6
+        A.asrkf_stats_reset(ctx)
+        assert len(A.asrkf_timing_series(ctx)) == 0
+        assert A.asrkf_stats(ctx)["attn_launches"] == 0
+    finally:
+        A.asrkf_destroy(ctx)
+
+
+def _config_of(A, w):
+    return A.make_config(w.n_layers, w.batch, w.n_q_heads, w.n_kv_heads, w.head_dim, w.max_ctx,
+                         w.window_K, w.tau, w.k_soft, w.vocab, entropy_spike=w.entropy_spike,
+                         conf_drop=w.conf_drop, wr_last_N=w.wr_last_N, dtype=w.dtype,
+                         spill_min_D=w.spill_min_D, device_rows=w.device_rows,
+                         history_W=w.history_W, relevance=w.relevance, scope=w.scope,
+                         candidates=w.candidates)
+
+
+@pytest.mark.parametrize("spill", [False, True], ids=["resident", "spill"])
+def test_reset_context_runs_like_a_fresh_one(spill):
+    """A context that ran another batch (other prompts and lengths, recoveries)
+    and was reset runs a workload bit for bit like a fresh context: outputs,
+    token states, monitor and counters at every step."""
+    import paper_2512_11221_amd as A
+    w = gen.Workload(name="reset-hh", seed=gen.SEED + 97, n_layers=2, batch=2, n_q_heads=32,
+                     n_kv_heads=8, head_dim=128, dtype="bf16", prefill=[300, 170], steps=24,
+                     window_K=16, tau=0.5, k_soft=2.0, vocab=1024, logit_sigma=2.0, recipe="hh",
+                     f_hh=[0.35, 0.25], entropy_spike=6.5, flat_logit_steps=(12, 13),
+                     spill_min_D=2 if spill else 0)
+    s_cold, s_hot = gen.hh_relevance_bounds(w)
+    assert s_cold < w.tau - H.MARGIN and s_hot > w.tau + H.MARGIN
+    other = w.replace(name="reset-other", seed=gen.SEED + 98, prefill=[120, 250],
+                      max_ctx=w.max_ctx, flat_logit_steps=(5, 6, 7))
+    inst = [(l, b) for l in range(2) for b in range(2)]
+    fresh, mon_f, st_f = H.run_gpu(w, H.Inputs(w), inst)
+    ctx = A.asrkf_init(_config_of(A, w))
+    try:
+        H.run_gpu(other, H.Inputs(other), inst, steps=18, ctx=ctx)
+        A.asrkf_set_timing(ctx, True)
+        A.asrkf_reset(ctx)
+        st0 = A.asrkf_stats(ctx)
+        assert st0["step"] == 0 and st0["attended_total"] == 0 and st0["attn_launches"] == 0
+        assert st0["recoveries"] == [0, 0, 0, 0] and st0["rr_requests"] == 0
+        again, mon_a, st_a = H.run_gpu(w, H.Inputs(w), inst, ctx=ctx)
+        assert A.asrkf_stats(ctx)["attn_launches"] == 0          # reset turned timing off
+    finally:
+        A.asrkf_destroy(ctx)
+    for key in inst:
+        assert len(fresh[key]) == len(again[key]) == w.steps
+        for a, b in zip(fresh[key], again[key]):
+            for f in ("out", "unfreeze", "count", "frozen", "active"):
+                np.testing.assert_array_equal(a[f], b[f], err_msg=f"{key} step {a['t']} {f}")
+    assert mon_f == mon_a
+    for a, b in zip(st_f, st_a):
+        for k in ("step", "attended_total", "active_positions", "total_positions", "recoveries",
+                  "rr_requests", "rows_to_host", "rows_from_host", "rows_reused"):
+            assert a[k] == b[k], (k, a[k], b[k])
+    o = H.run_oracle(w, H.Inputs(w), inst)
+    for key in inst:
+        H.compare_instance(fresh[key], o[key])
