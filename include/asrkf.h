@@ -129,6 +129,12 @@ typedef struct {
     int32_t candidates;      /* ASRKF_CAND_OUTSIDE (0, Algorithm 1): active tokens at positions
                                 < n_t - window_K may freeze; ASRKF_CAND_INSIDE: active tokens at
                                 positions >= n_t - window_K may freeze instead */
+    float   debug_margin;    /* 0: off.  > 0: every freeze decision (an attended token that
+                                may freeze, per `candidates`) taken on a relevance within
+                                debug_margin of tau (|s_j - tau| < debug_margin, s_j as in
+                                Eq. 2; token scope: its mean over layers) is counted in
+                                asrkf_stats.margin_hits -- decisions that rounding can flip;
+                                a run whose scores keep that margin reports 0 */
 } asrkf_config;
 
 typedef struct {
@@ -148,6 +154,8 @@ typedef struct {
     int64_t rows_released;      /* spill mode: device rows given up by freezing tokens */
     int64_t rows_reused;        /* spill mode: restored tokens that took back their last device
                                    row, which still held their K and V (no copy) */
+    int64_t margin_hits;        /* debug_margin > 0: freeze decisions, over completed steps,
+                                   on a relevance within debug_margin of tau */
 } asrkf_stats_t;
 
 typedef struct asrkf_ctx asrkf_ctx;

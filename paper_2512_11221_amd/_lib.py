@@ -35,7 +35,7 @@ class asrkf_config(ctypes.Structure):
         ("dtype", ctypes.c_int32), ("spill_min_D", ctypes.c_int32),
         ("device_rows", ctypes.c_int32), ("history_W", ctypes.c_int32),
         ("relevance", ctypes.c_int32), ("scope", ctypes.c_int32),
-        ("candidates", ctypes.c_int32),
+        ("candidates", ctypes.c_int32), ("debug_margin", ctypes.c_float),
     ]
 
 
@@ -47,7 +47,7 @@ class asrkf_stats_t(ctypes.Structure):
         ("attn_launches", ctypes.c_int64), ("attn_kernel_ms", ctypes.c_double),
         ("compression", ctypes.c_double), ("rows_to_host", ctypes.c_int64),
         ("rows_from_host", ctypes.c_int64), ("rows_released", ctypes.c_int64),
-        ("rows_reused", ctypes.c_int64),
+        ("rows_reused", ctypes.c_int64), ("margin_hits", ctypes.c_int64),
     ]
 
     def as_dict(self):
@@ -140,7 +140,7 @@ def _enum(name, value, names):
 def make_config(n_layers, batch, n_q_heads, n_kv_heads, head_dim, max_ctx, window_K, tau,
                 k_soft, vocab, entropy_spike=math.inf, conf_drop=0.0, wr_last_N=0,
                 dtype="bf16", spill_min_D=0, device_rows=0, history_W=0, relevance="abs",
-                scope="layer", candidates="outside"):
+                scope="layer", candidates="outside", debug_margin=0.0):
     return asrkf_config(n_layers, batch, n_q_heads, n_kv_heads, head_dim, max_ctx, window_K,
                         tau, k_soft, vocab, entropy_spike, conf_drop, wr_last_N,
                         _enum("dtype", dtype, {"bf16": BF16, "f32": F32}),
@@ -148,7 +148,7 @@ def make_config(n_layers, batch, n_q_heads, n_kv_heads, head_dim, max_ctx, windo
                         _enum("relevance", relevance, {"abs": REL_ABS, "softmax": REL_SOFTMAX}),
                         _enum("scope", scope, {"layer": SCOPE_LAYER, "token": SCOPE_TOKEN}),
                         _enum("candidates", candidates,
-                              {"outside": CAND_OUTSIDE, "inside": CAND_INSIDE}))
+                              {"outside": CAND_OUTSIDE, "inside": CAND_INSIDE}), debug_margin)
 
 
 def asrkf_init(cfg):

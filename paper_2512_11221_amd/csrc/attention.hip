@@ -465,8 +465,10 @@ attention_kernel(AttnArgs a) {
                                 rel_lds[(tb + u * TPI + tk) * NWG + wpart] = rel;
                             } else if (scope_token) {
                                 rel_lds[tb + u * TPI + tk] = rel;
-                            } else if (rel < a.tau_H) {   // the freeze loop picks the candidates
-                                flag_lds[tb + u * TPI + tk] = 1;
+                            } else {                      // the freeze loop picks the candidates
+                                const int f = (rel < a.tau_H ? 1 : 0) |
+                                              (fabsf(rel - a.tau_H) < a.margin_H ? 2 : 0);
+                                if (f) flag_lds[tb + u * TPI + tk] = (uint8_t)f;
                             }
                         }
                     }
@@ -537,7 +539,9 @@ attention_kernel(AttnArgs a) {
 #pragma unroll
                         for (int p2 = 0; p2 < NWG; ++p2) sum += rel_lds[i * NWG + p2];
                         if (scope_token) rel_lds[i * NWG] = sum;
-                        else flag_lds[i] = rel_abs && sum < a.tau_H;
+                        else flag_lds[i] = rel_abs ? (uint8_t)((sum < a.tau_H ? 1 : 0) |
+                                                               (fabsf(sum - a.tau_H) < a.margin_H ? 2 : 0))
+                                                   : (uint8_t)0;
                     }
                 }
             }

@@ -81,16 +81,24 @@ __device__ __forceinline__ Ladder make_ladder(const CompactArgs& a, int b, int n
 // updates the detection bits of a flagged position.  Returns whether u changed.
 __device__ __forceinline__ bool freeze4(const CompactArgs& a, const int32_t* dur_lds, size_t base,
                                         int p, int hi, int n, int (&u)[4], const int (&cnt)[4],
-                                        uint32_t flags, const float (&rel)[4]) {
+                                        uint32_t flags, const float (&rel)[4], int& near) {
     if (!a.freeze) return false;
     bool dirty = false;
     const bool inside = a.cand_inside != 0;
 #pragma unroll
     for (int k = 0; k < 4; ++k) {
         const int q = p + k;
-        bool low;
-        if (a.scope_token) low = rel[k] < a.tau_LH;
-        else low = ((flags >> (8 * k)) & 0xFFu) != 0;
+        bool low, close;
+        if (a.scope_token) {
+            low = rel[k] < a.tau_LH;
+            close = fabsf(rel[k] - a.tau_LH) < a.margin_LH;
+        } else {
+            low = ((flags >> (8 * k)) & 1u) != 0;
+            close = ((flags >> (8 * k)) & 2u) != 0;
+        }
+        // debug margin: a freeze decision of step t (an attended candidate) on a
+        // score near tau
+        near += (q < hi && u[k] <= a.t && close && freeze_candidate(q, n - a.window_K, inside)) ? 1 : 0;
         if (q < hi && u[k] <= a.t && low && freeze_candidate(q, n - a.window_K, inside)) {
             int c;
             if (a.history_W == 0) {
@@ -111,6 +119,14 @@ __device__ __forceinline__ bool freeze4(const CompactArgs& a, const int32_t* dur
         }
     }
     return dirty;
+}
+
+// Debug margin: the decisions near tau a thread counted, added to the
+// context's counter (one atomic per wave).  Every thread of the wave calls it.
+__device__ __forceinline__ void add_margin_hits(const CompactArgs& a, int near) {
+    if (!a.margin_hits) return;               // uniform
+    for (int o = 32; o > 0; o >>= 1) near += __shfl_xor(near, o);
+    if ((threadIdx.x & 63) == 0 && near) atomicAdd(a.margin_hits, (unsigned long long)near);
 }
 
 // Eq. 3 durations of the counts below kDurLds, staged in LDS by every
@@ -246,7 +262,7 @@ __device__ int compact_range(const CompactArgs& a, const Ladder& r, const int32_
     int32_t* U = a.unfreeze + base;
     int32_t* list = a.list + base;
     const int tid = threadIdx.x;
-    int listed = 0;
+    int listed = 0, near = 0;
     Tile4 next;
     if constexpr (MODE != 2) load_tile(a, base, lo + 4 * tid, next);
     else load_u(U, lo + 4 * tid, a.cap, next.u);
@@ -260,7 +276,7 @@ __device__ int compact_range(const CompactArgs& a, const Ladder& r, const int32_
         }
         bool flag[4];
         if constexpr (MODE != 2) {
-            bool dirty = freeze4(a, dur_lds, base, p, hi, n, u, cur.c, cur.f, cur.r);
+            bool dirty = freeze4(a, dur_lds, base, p, hi, n, u, cur.c, cur.f, cur.r, near);
 #pragma unroll
             for (int k = 0; k < 4; ++k) {
                 bool hit;
@@ -287,6 +303,7 @@ __device__ int compact_range(const CompactArgs& a, const Ladder& r, const int32_
         }
         listed += sc.tot0;
     }
+    if constexpr (MODE != 2) add_margin_hits(a, near);
     return listed;
 }
 
@@ -538,14 +555,14 @@ compact_spill_kernel(CompactArgs a) {
 
     // pass 1: the freeze loop, recovery, releases (out-list), take-backs, and the
     // number of positions that need a row
-    int n_out = 0, released = 0, back = 0, need = 0;
+    int n_out = 0, released = 0, back = 0, need = 0, near = 0;
     for (int p0 = 0; p0 < n; p0 += 4 * kThreads) {
         const int p = p0 + 4 * tid;
         Tile4 cur;
         load_tile(a, base, p, cur);
         mask_tile(cur, p, n);
         int (&u)[4] = cur.u;
-        bool dirty = freeze4(a, dur_lds, base, p, n, n, u, cur.c, cur.f, cur.r);
+        bool dirty = freeze4(a, dur_lds, base, p, n, n, u, cur.c, cur.f, cur.r, near);
 #pragma unroll
         for (int k = 0; k < 4; ++k) {
             bool hit;
@@ -581,6 +598,8 @@ compact_spill_kernel(CompactArgs a) {
 
     // the rows for the positions that need one, and one for the next token
     const int popped = find_free_rows(a, inst, need + 1, tot0, tot1, &last_idx);
+
+    add_margin_hits(a, near);
 
     // pass 2: the active list of step t+1 and the device row of every entry
     int listed = 0, pn_run = 0;
@@ -652,7 +671,7 @@ spill_count_kernel(CompactArgs a) {
     const Ladder r = make_ladder(a, b, n);
     const size_t base = (size_t)inst * a.cap;
     int32_t* U = a.unfreeze + base;
-    int nl = 0, nf = 0;
+    int nl = 0, nf = 0, near = 0;
     for (int p0 = lo; p0 < hi; p0 += 4 * kThreads) {
         const int p = p0 + 4 * threadIdx.x;
         Tile4 cur;
@@ -661,7 +680,7 @@ spill_count_kernel(CompactArgs a) {
         int (&u)[4] = cur.u;
         int row[4];
         load4(a.row_of + base, p, hi, row, -1);
-        bool dirty = freeze4(a, dur_lds, base, p, hi, n, u, cur.c, cur.f, cur.r);
+        bool dirty = freeze4(a, dur_lds, base, p, hi, n, u, cur.c, cur.f, cur.r, near);
         bool listed[4], first[4];
 #pragma unroll
         for (int k = 0; k < 4; ++k) {
@@ -683,6 +702,7 @@ spill_count_kernel(CompactArgs a) {
         nl += sc.tot0;
         nf += sc.tot1;
     }
+    add_margin_hits(a, near);
     if (threadIdx.x == 0) {
         SegCounts* rec = seg_records(a, inst);
         rec[seg].listed = nl;

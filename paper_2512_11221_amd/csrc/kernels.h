@@ -55,9 +55,10 @@ struct AttnArgs {
     const int32_t* list_row;  // layer base, [B][cap] device row of each listed position
                               // (spill mode only; in resident mode the row is the position)
     const int32_t* n_active;  // layer base, [B]
-    uint8_t* flag;            // layer base, [B][cap]: 1 where the attended position scores
-                              // below tau (Eq. 2), 0 where not; read by the freeze loop
-                              // at the end of the step
+    uint8_t* flag;            // layer base, [B][cap]: bit 0 set where the attended position
+                              // scores below tau (Eq. 2), bit 1 where the score lies within
+                              // the debug margin of tau; read by the freeze loop at the
+                              // end of the step
     int32_t* t_dev;           // first layer of a step: advanced by one (steps started), else null
     float* part_acc;          // [grid + B][Hq][D]
     float* part_ml;           // [grid + B][Hq][2]: (max in log2 units, sum)
@@ -67,6 +68,8 @@ struct AttnArgs {
     int32_t pool_rows;        // device rows per sequence (cap in resident mode)
     int32_t spill;            // 1: rows come from list_row
     float tau_H;              // tau * Hq: compared against sum_h |q_h . k_j|
+    float margin_H;           // debug margin * Hq (0: off): a score this close to tau_H
+                              // also sets bit 1 of the position's flag
     float scale_log2;         // log2(e) / sqrt(D)
     // relevance reading and state scope
     int32_t rel_mode;         // 0: Eq. 2 |q.k| scored here; 1: softmax weights (weight_relevance_kernel)
@@ -98,7 +101,7 @@ struct RelevanceArgs {
     uint8_t* flag;            // state base [B][cap]
     float* rel_acc;           // token scope [B][cap]
     int32_t B, cap, Hq, scope_token, first_layer;
-    float tau_H;
+    float tau_H, margin_H;
 };
 
 struct CompactArgs {
@@ -141,6 +144,8 @@ struct CompactArgs {
     int32_t scope_token;      // 1: one state per sequence, scored by the sum over layers
     const float* rel_acc;     // [B][cap] token scope: relevance summed over layers and heads
     float tau_LH;             // tau * n_layers * Hq
+    float margin_LH;          // token scope: debug margin * n_layers * Hq
+    unsigned long long* margin_hits;  // debug margin on: decisions near tau are counted here
     int32_t* count;           // [L][B][cap] (or [B][cap] in token scope): c_j
     uint64_t* hmask;
     int32_t* hlast;

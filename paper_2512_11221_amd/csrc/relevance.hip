@@ -34,7 +34,7 @@ weight_relevance_kernel(RelevanceArgs a) {
         const int pos = a.list[row + i];
         const size_t o = row + pos;
         if (a.scope_token) a.rel_acc[o] = a.first_layer ? s : a.rel_acc[o] + s;
-        else a.flag[o] = s < a.tau_H ? 1 : 0;
+        else a.flag[o] = (s < a.tau_H ? 1 : 0) | (fabsf(s - a.tau_H) < a.margin_H ? 2 : 0);
     }
 }
 

@@ -118,7 +118,8 @@ struct asrkf_ctx {
     float* ent_partial = nullptr;   // [B][kEntropySplitMax][3]
     int32_t* ent_ticket = nullptr;  // [B]
     unsigned long long* counters = nullptr;   // [0] listed_total, [1..3] recoveries, [5] rr,
-                                              // [8] rows to host, [9] rows from host, [10] released
+                                              // [8] rows to host, [9] rows from host, [10] released,
+                                              // [11] rows taken back, [12] margin hits
 
     // relevance reading and state scope
     bool token_scope = false;     // one token state per sequence (state_layers = 1)
@@ -266,6 +267,8 @@ asrkf_status validate(const asrkf_config* c) {
     if (!valid_k(c->k_soft)) return fail(ASRKF_EINVAL, "k_soft must be in [2^-8, 2^16]");
     if (c->vocab < 1) return fail(ASRKF_EINVAL, "vocab must be >= 1");
     if (isnan(c->entropy_spike) || isnan(c->conf_drop)) return fail(ASRKF_EINVAL, "NaN threshold");
+    if (!(c->debug_margin >= 0.f) || isinf(c->debug_margin))
+        return fail(ASRKF_EINVAL, "debug_margin must be finite and >= 0");
     if (c->dtype != ASRKF_BF16 && c->dtype != ASRKF_F32) return fail(ASRKF_EINVAL, "unknown dtype");
     if (c->spill_min_D < 0) return fail(ASRKF_EINVAL, "spill_min_D must be >= 0");
     if (c->history_W < 0 || c->history_W > 64) return fail(ASRKF_EINVAL, "history_W must be in 0..64");
@@ -581,6 +584,8 @@ asrkf_status build_lists(asrkf_ctx* ctx, int forced_level, hipStream_t s) {
     a.scope_token = ctx->token_scope ? 1 : 0;
     a.rel_acc = ctx->rel_acc;
     a.tau_LH = ctx->cfg.tau * (float)ctx->cfg.n_layers * (float)ctx->cfg.n_q_heads;
+    a.margin_LH = ctx->cfg.debug_margin * (float)ctx->cfg.n_layers * (float)ctx->cfg.n_q_heads;
+    a.margin_hits = ctx->cfg.debug_margin > 0.f ? ctx->counters + 12 : nullptr;
     a.count = ctx->count;
     a.hmask = ctx->hmask;
     a.hlast = ctx->hlast;
@@ -772,6 +777,7 @@ asrkf_status decode_step_impl(asrkf_ctx* ctx, int32_t layer, const void* q, cons
     a.Hq = c.n_q_heads;
     a.Hkv = c.n_kv_heads;
     a.tau_H = c.tau * (float)c.n_q_heads;
+    a.margin_H = c.debug_margin * (float)c.n_q_heads;
     a.scale_log2 = (float)(1.4426950408889634 / sqrt((double)c.head_dim));
 
     std::pair<hipEvent_t, hipEvent_t> ev{nullptr, nullptr};
@@ -814,6 +820,7 @@ asrkf_status decode_step_impl(asrkf_ctx* ctx, int32_t layer, const void* q, cons
         r.scope_token = a.scope_token;
         r.first_layer = a.first_layer;
         r.tau_H = a.tau_H;
+        r.margin_H = a.margin_H;
         HIP_OK(ctx, launch_weight_relevance(r, s));
     }
 
@@ -961,6 +968,7 @@ asrkf_status asrkf_stats(asrkf_ctx* ctx, asrkf_stats_t* out) {
     out->rows_from_host = (int64_t)cnt[9];
     out->rows_released = (int64_t)cnt[10];
     out->rows_reused = (int64_t)cnt[11];
+    out->margin_hits = (int64_t)cnt[12];
     return ASRKF_OK;
 }
 
