@@ -49,12 +49,57 @@ def parse():
                     help="run only the first N layers of the workload (counter runs); 0 = all")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",
                     help="after the run, one plain device copy of BYTES (counter calibration)")
+    ap.add_argument("--summarize-trace", metavar="TRACE_DIR",
+                    help="print, from a rocprofv3 --kernel-trace --stats run of this bench (same "
+                         "--steps, --warmup and --layers), the kernel table and the attention "
+                         "kernel's mean duration over the measured steps of each pass; no GPU work")
     ap.add_argument("--summarize-counters", nargs=3, metavar=("FETCH_DIR", "WRITE_DIR", "BENCH_LOG"),
                     help="print the HBM traffic per attention launch from two rocprofv3 --pmc "
                          "runs (FETCH_SIZE, WRITE_SIZE) made with --copy-calibration, and its "
                          "ratio to the algorithmic bytes in the JSON line that the FETCH_SIZE "
                          "run printed (BENCH_LOG); no GPU work")
     return ap.parse_args()
+
+
+PASSES = ("rate", "steps", "kernel", "count")
+
+
+def summarize_trace(trace_dir, layers, warmup, steps):
+    """The kernel table of a rocprofv3 --stats run of this bench, and per pass
+    (in launch order: rate, steps, kernel, count) the mean duration of the
+    attention launches of the measured steps (each pass launches
+    (warmup + steps) x layers of them), split at the midpoint between the
+    shortest and longest launch (sparse below, dense above).  The profiler's
+    own timestamps; passes with HIP events under the profiler also show the
+    profiler's gaps around the dispatch, not inside it."""
+    import csv
+    import glob
+    import statistics as st
+    trace = glob.glob(os.path.join(trace_dir, "**", "*kernel_trace.csv"), recursive=True)[0]
+    stats = glob.glob(os.path.join(trace_dir, "**", "*kernel_stats.csv"), recursive=True)
+    out = {"kernels": []}
+    if stats:
+        for r in csv.DictReader(open(stats[0])):
+            out["kernels"].append({"name": r["Name"], "calls": int(r["Calls"]),
+                                   "avg_us": float(r["AverageNs"]) / 1e3,
+                                   "share": float(r["Percentage"]) / 100})
+    rows = [r for r in csv.DictReader(open(trace)) if "attention_kernel" in r["Kernel_Name"]]
+    rows.sort(key=lambda r: int(r["Start_Timestamp"]))
+    dur = [(int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3 for r in rows]
+    per = (warmup + steps) * layers
+    if len(dur) % per:
+        raise SystemExit(f"{len(dur)} attention launches is not a whole number of passes of {per}")
+    out["passes"] = {}
+    for i in range(len(dur) // per):
+        w = dur[i * per:(i + 1) * per][warmup * layers:]
+        mid = (min(w) + max(w)) / 2
+        sp = [x for x in w if x < mid]
+        de = [x for x in w if x >= mid]
+        out["passes"][PASSES[i] if i < len(PASSES) else str(i)] = {
+            "launches": len(w), "avg_us": st.mean(w),
+            "sparse": {"launches": len(sp), "avg_us": st.mean(sp)} if sp else None,
+            "dense": {"launches": len(de), "avg_us": st.mean(de)} if de else None}
+    return out
 
 
 def summarize_counters(fetch_dir, write_dir, bench_log, timed, copy_bytes):
@@ -220,6 +265,12 @@ def cpu_baseline(w, budget_s):
 
 def main():
     args = parse()
+    if args.summarize_trace:
+        layers = args.layers or getattr(__import__("synth.gen", fromlist=["gen"]),
+                                        WORKLOADS[args.workload])().n_layers
+        print(json.dumps(summarize_trace(args.summarize_trace, layers, args.warmup, args.steps),
+                         indent=1))
+        return
     if args.summarize_counters:
         print(json.dumps(summarize_counters(*args.summarize_counters, args.steps,
                                             args.copy_calibration or (1 << 30)), indent=1))
