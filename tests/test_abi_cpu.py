@@ -112,3 +112,33 @@ def test_c_program_uses_the_abi(tmp_path):
     r = subprocess.run([exe], capture_output=True, text=True, timeout=60)
     assert r.returncode == 0, r.stderr
     assert "C ABI checks passed" in r.stdout
+
+
+def test_binding_structs_match_the_header(tmp_path):
+    """The ctypes mirrors of asrkf_config and asrkf_stats_t have the size and
+    field offsets the C compiler gives the header's structs (a field added to
+    the header and not to the binding, or the reverse, fails here)."""
+    import ctypes
+    import shutil
+    import subprocess
+    gcc = shutil.which("gcc")
+    if gcc is None:
+        pytest.skip("no C compiler")
+    from paper_2512_11221_amd import _lib as L
+    lines = ["#include <stddef.h>", "#include <stdio.h>", '#include "asrkf.h"', "int main(void) {"]
+    for cname, py in (("asrkf_config", L.asrkf_config), ("asrkf_stats_t", L.asrkf_stats_t)):
+        lines.append(f'    printf("{cname} size %zu\\n", sizeof({cname}));')
+        for field, _ in py._fields_:
+            lines.append(f'    printf("{cname} {field} %zu\\n", offsetof({cname}, {field}));')
+    lines += ["    return 0;", "}"]
+    src = tmp_path / "layout.c"
+    src.write_text("\n".join(lines) + "\n")
+    exe = str(tmp_path / "layout")
+    subprocess.run([gcc, "-std=c99", "-Wall", "-Werror", str(src), "-I", os.path.join(ROOT, "include"),
+                    "-o", exe], check=True, capture_output=True, text=True)
+    out = subprocess.run([exe], capture_output=True, text=True, timeout=60).stdout.split("\n")
+    got = {(a, b): int(c) for a, b, c in (x.split() for x in out if x)}
+    for cname, py in (("asrkf_config", L.asrkf_config), ("asrkf_stats_t", L.asrkf_stats_t)):
+        assert got[(cname, "size")] == ctypes.sizeof(py), cname
+        for field, _ in py._fields_:
+            assert got[(cname, field)] == getattr(py, field).offset, (cname, field)

@@ -123,8 +123,14 @@ def test_c_program_drives_the_gpu():
     its own double-precision attention, plus the statistics."""
     import os
     import subprocess
-    exe = os.path.join(os.path.dirname(os.path.abspath(__file__)), "c_abi", "abi_gpu_check")
+    here = os.path.dirname(os.path.abspath(__file__))
+    exe = os.path.join(here, "c_abi", "abi_gpu_check")
     assert os.path.exists(exe), "build it first: __graft_entry__.build()"
+    for src in (os.path.join(here, "c_abi", "abi_gpu_check.c"),
+                os.path.join(here, "..", "include", "asrkf.h")):
+        # a program built against an older header would pass a struct of the old layout
+        assert os.path.getmtime(exe) >= os.path.getmtime(src), \
+            f"{exe} is older than {src}: rebuild it with __graft_entry__.build()"
     r = subprocess.run([exe], capture_output=True, text=True, timeout=120)
     assert r.returncode == 0, r.stdout + r.stderr
     assert "C ABI GPU run passed" in r.stdout
