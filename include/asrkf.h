@@ -11,9 +11,10 @@
  *
  * decode_step is Algorithm 1 up to and including the freeze loop for one
  * layer of every sequence (attention over the active cache, Eq. 1; relevance,
- * Eq. 2; freeze schedule, Eq. 3).  restore is the rest of the step: entropy
- * monitoring and staged recovery (Sec. 3.6), then the timer loop and the
- * rebuild of every active cache for the next step (Sec. 3.5).
+ * Eq. 2; the freeze verdicts).  restore is the rest of the step: entropy
+ * monitoring and staged recovery (Sec. 3.6), the freeze schedule of the step's
+ * verdicts (Eq. 3), then the timer loop and the rebuild of every active cache
+ * for the next step (Sec. 3.5).
  *
  * Conventions for every call:
  *  - Pointers named "device" must point to GPU memory of the current HIP
@@ -177,9 +178,12 @@ asrkf_status asrkf_prefill(asrkf_ctx* ctx, int32_t layer, int32_t seq,
 
 /* Algorithm 1 up to the end of the freeze loop, for one layer of every
  * sequence: append the new token, attend over the active cache (Eq. 1),
- * score every attended token (Eq. 2), and freeze low-relevance tokens outside
- * the window of the window_K most recent positions (inside it with
- * ASRKF_CAND_INSIDE) for the durations of Eq. 3.
+ * score every attended token (Eq. 2), and decide which low-relevance tokens
+ * outside the window of the window_K most recent positions (inside it with
+ * ASRKF_CAND_INSIDE) freeze.  Their counts and Eq. 3 durations are applied to
+ * the token states by asrkf_restore, before recovery, in one pass over every
+ * layer's states; the states after restore are Algorithm 1's at the end of
+ * the step.
  *   q:     device, [batch][n_q_heads][head_dim] of cfg.dtype
  *   k_new: device, [batch][n_kv_heads][head_dim] of cfg.dtype
  *   v_new: device, same layout as k_new
@@ -210,8 +214,10 @@ asrkf_status asrkf_decode_step_static(asrkf_ctx* ctx, int32_t layer, const void*
                                       void* stream);
 
 /* End the step: entropy of each sequence's next-token distribution and the
- * recovery ladder (Sec. 3.6), then the timer loop and the active caches of
- * the next step (Algorithm 1 timer loop; Sec. 3.5).
+ * recovery ladder (Sec. 3.6), the step's freeze schedule (c_j += 1 and the
+ * Eq. 3 duration for every token the step's decode_step calls found below
+ * tau), the recovery level applied, then the timer loop and the active caches
+ * of the next step (Algorithm 1 timer loop; Sec. 3.5).
  *   logits: device, [batch][vocab] float32, or NULL (no entropy; AUTO then
  *           applies no recovery)
  *   mode:   an asrkf_recover value; a forced level applies to every sequence;
