@@ -294,7 +294,13 @@ attention_kernel(AttnArgs a) {
             a.slot_end[b] = x1 > x0 ? group_of(x1 - 1, T, Gn) + b + 1 : 0;
         }
     }
-    const int w = blockIdx.x;
+    // the range this workgroup takes.  Workgroups are dealt to the 8 XCDs round
+    // robin; when every workgroup has a range, each XCD takes a contiguous block
+    // of ranges (measured: the slowest XCD's share ends sooner).  Any one-to-one
+    // map gives the same partials, so the results do not depend on it; with
+    // fewer ranges than workgroups the ranges stay spread over the XCDs.
+    const bool blocked = Gn == (int)gridDim.x && gridDim.x % 8 == 0;
+    const int w = blocked ? (int)((blockIdx.x % 8) * (gridDim.x / 8) + blockIdx.x / 8) : (int)blockIdx.x;
     if (w >= Gn) return;
 
     const int wave = wave_uniform(threadIdx.x >> 6);
