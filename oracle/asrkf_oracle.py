@@ -36,7 +36,10 @@ design notes with the evidence for it):
   |q . k|; token-global scope (one token state per sequence shared by all
   layers, relevance averaged over layers) instead of per-(layer, sequence)
   states; freeze candidates taken inside the window of the K most recent
-  positions (the wording of Sec. 3.2) instead of outside it;
+  positions (the wording of Sec. 3.2) instead of outside it.  Which state
+  scope the paper means is fixed by no printed value (every flagged token
+  gives the same counts in both scopes): parity unpinned for that reading,
+  while each scope's own functions are pinned by their reductions;
 * recovery (the paper proposes but never evaluates it, so no printed value
   pins it; hand-derived expected states under these readings do):
   a step whose entropy exceeds theta_H (or whose top probability falls below
