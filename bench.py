@@ -393,11 +393,12 @@ def main():
 
     # The step rate comes from a pass without instrumentation.  The same steps
     # are then replayed three more times on the same context (reset in between,
-    # so every pass reads and writes the same device memory): with a HIP event between steps (each
-    # step's GPU time), with HIP events recorded by every attention dispatch
-    # (the kernel's execution time per launch, for the roofline), and with the
-    # counters read after every step (attended token-layers per step).  None of
-    # the measured passes waits on the host inside its loop.
+    # so every pass reads and writes the same device memory): with a HIP event
+    # between steps (each step's GPU time), with HIP events recorded by every
+    # attention dispatch (the kernel's execution time per launch, for the
+    # roofline), and with the counters read after every step (attended
+    # token-layers per step).  Only the last pass waits on the host inside its
+    # loop, and it times nothing.
     elapsed, st, _ = run_pass("rate")
     _, _, s_steps = run_pass("steps")
     _, st_timed, s_kernel = run_pass("kernel")
