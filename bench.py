@@ -272,7 +272,8 @@ def main():
                          indent=1))
         return
     if args.summarize_counters:
-        print(json.dumps(summarize_counters(*args.summarize_counters, args.steps,
+        # the measured steps of the counter runs' last pass: one attention launch per layer
+        print(json.dumps(summarize_counters(*args.summarize_counters, args.steps * max(1, args.layers),
                                             args.copy_calibration or (1 << 30)), indent=1))
         return
     if args.graph and args.warmup < 1:

@@ -72,6 +72,12 @@ def load():
         return _lib
     if not os.path.exists(LIB_PATH):
         raise ImportError(f"{LIB_PATH} is not built; run __graft_entry__.build()")
+    # torch brings a HIP runtime of its own.  The library must use the same one
+    # as the tensors it is given, so torch's is loaded and started first: with
+    # the library loaded first, the two runtimes have been seen to disagree
+    # (workgroup occupancy reported as zero, torch finding no GPU).
+    import torch
+    torch.cuda.is_available()
     lib = ctypes.CDLL(LIB_PATH)
     P, I32, F = ctypes.c_void_p, ctypes.c_int32, ctypes.c_float
     sig = {

@@ -242,7 +242,20 @@ constexpr bool merge_one_round() {
     return (size_t)kWaves * (2 * G + G * Row<BF16, D>::kPerLane) * 64 * 4 <= 148 * 1024;
 }
 
+// Shapes whose first tile can come from the plan records: one token per wave
+// iteration, one wave per token, the first tiles of all waves within the
+// record's positions.
 template <bool BF16, int D, int G, int HKV>
+constexpr bool prefetch_shape() {
+    constexpr int VH = HKV * split_of<BF16, D, G>();
+    constexpr int NWG = VH > 8 ? VH / 8 : 1;
+    constexpr int TPI = 8 / (VH > 8 ? 8 : VH);
+    return TPI == 1 && NWG == 1 && kWaves * tile_unroll<BF16, D>() <= kPlanTokens;
+}
+
+// PF: the first tile of a range's first chunk is requested from the plan
+// record (a.plan must be set); without it the kernel never reads a.plan.
+template <bool BF16, int D, int G, int HKV, bool PF>
 __global__ void __launch_bounds__(64 * kWaves)
 attention_kernel(AttnArgs a) {
     using R = Row<BF16, D>;
@@ -282,6 +295,30 @@ attention_kernel(AttnArgs a) {
     // the step's first launch advances the device step counter that the
     // end-of-step rebuild reads (a graph replay of the step then sees its step)
     if (a.t_dev && blockIdx.x == 0 && threadIdx.x == 0) *a.t_dev += 1;
+    // The first-tile record of the range this workgroup takes when every
+    // workgroup has one (checked once the ranges are known), requested
+    // together with the counts: with it the first K/V rows are requested
+    // before the chunk's positions and q arrive.
+    constexpr bool kPrefetch = PF && prefetch_shape<BF16, D, G, HKV>();
+    static_assert(!kPrefetch || (TPI == 1 && NWG == 1 && kGroups * TT <= kPlanTokens), "record layout");
+    const int w_full = gridDim.x % 8 == 0 ? (int)((blockIdx.x % 8) * (gridDim.x / 8) + blockIdx.x / 8)
+                                          : (int)blockIdx.x;
+    int rec_b = -1, rec_i0 = 0, rec_len = 0;
+    int rec_pos[kUnroll] = {};
+    if constexpr (kPrefetch) {
+        // a.plan is always set for this variant; the test stays: without it the
+        // compiler scheduled the tile loop differently and the launch took 1.3 %
+        // longer (interleaved runs)
+        if (a.plan) {
+            const int32_t* rec = a.plan + (size_t)w_full * kPlanInts;
+            const int t0 = 4 + wave_uniform(threadIdx.x >> 6) * TT;
+            rec_b = rec[0];
+            rec_i0 = rec[1];
+            rec_len = rec[2];
+#pragma unroll
+            for (int u = 0; u < kUnroll; ++u) rec_pos[u] = rec[t0 + u];
+        }
+    }
     plan_ranges(a.n_active, a.B, seq_off);
     __syncthreads();
     const int T = wave_uniform(seq_off[a.B]);
@@ -327,6 +364,7 @@ attention_kernel(AttnArgs a) {
         }
         b = l0;
     }
+    bool first_piece = true;
     while (x < x_end) {
         while (wave_uniform(seq_off[b + 1]) <= x) ++b;   // skip empty lists
         const int sb = wave_uniform(seq_off[b]) + kSeqCost;   // the list's first real token
@@ -359,6 +397,14 @@ attention_kernel(AttnArgs a) {
 
         for (int c0 = i0; c0 < i1; c0 += kChunk) {
             const int len = min(kChunk, i1 - c0);
+            // the first tile of the range's first chunk comes from the record when it
+            // describes this chunk and the tile does not reach the appended token
+            uint4 kp[kUnroll][NC], vp[kUnroll][NC];
+            bool have = false;
+            if constexpr (kPrefetch)
+                have = first_piece && c0 == i0 && w == w_full && b == wave_uniform(rec_b) &&
+                       i0 == wave_uniform(rec_i0) && len == wave_uniform(rec_len) && wgrp * TT < len &&
+                       c0 + kGroups * TT < nb && !spill;
             // a chunk that ends with the new token appends its row to the cache
             // (a token row is at most 8 heads x 128 x 4 bytes, one 16-byte piece
             // per thread); its loads overlap the staging loads below
@@ -381,11 +427,11 @@ attention_kernel(AttnArgs a) {
                 int sp[kStage], sr[kStage];
 #pragma unroll
                 for (int k = 0; k < kStage; ++k) {
-                    const int i = threadIdx.x + k * 64 * kWaves;
-                    if (i < len) {
-                        sp[k] = list_b[c0 + i];
-                        if (spill) sr[k] = lrow_b[c0 + i];
-                    }
+                    // every load issued (the last entry past the chunk's end), so the
+                    // waits below count loads instead of waiting for all of them
+                    const int i = min((int)threadIdx.x + k * 64 * kWaves, len - 1);
+                    sp[k] = list_b[c0 + i];
+                    if (spill) sr[k] = lrow_b[c0 + i];
                 }
                 const __amdgpu_buffer_rsrc_t rq = __builtin_amdgcn_make_buffer_rsrc(
                     (void*)((const char*)a.q + (size_t)b * a.Hq * R::kBytes), (short)0, a.Hq * R::kBytes,
@@ -397,6 +443,25 @@ attention_kernel(AttnArgs a) {
                     for (int c = 0; c < NC; ++c)
                         qr[h][c] = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(
                             rq, qo + h * R::kBytes + c * 128, 0, 0));
+                // the first tile's rows, requested after the staging loads so that the
+                // staging waits for those only (rows of tokens past the chunk's end: the
+                // tile's first token, as in the tile loop).  Without a record the loads
+                // are still issued, at an offset past the cache's range (a sequence's
+                // rows stay below 2 GiB): they return zeros without a memory access,
+                // and the waits are counted alike on both paths.
+                if constexpr (kPrefetch) {
+#pragma unroll
+                    for (int u = 0; u < kUnroll; ++u) {
+                        const int li = wgrp * TT + u < len ? u : 0;
+                        const int so = have ? wave_uniform(rec_pos[li]) * row_stride : 0;
+#pragma unroll
+                        for (int c = 0; c < NC; ++c) {
+                            const int vo = have ? lane_off + c * 128 : (int)0x80000000;
+                            kp[u][c] = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(rk, vo, so, kStreamPolicy));
+                            vp[u][c] = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(rv, vo, so, kStreamPolicy));
+                        }
+                    }
+                }
 #pragma unroll
                 for (int k = 0; k < kStage; ++k) {
                     const int i = threadIdx.x + k * 64 * kWaves;
@@ -416,26 +481,13 @@ attention_kernel(AttnArgs a) {
             __threadfence_block();
             __syncthreads();
 
-            for (int tb = wgrp * TT; tb < len; tb += kGroups * TT) {
-                uint4 kr[kUnroll][NC], vr[kUnroll][NC];
+            // One tile: rows kr, vr of the tokens from tb on (rows of tokens past the
+            // chunk's end are the tile's first token's, masked here).
+            auto tile = [&](const uint4 (&kr)[kUnroll][NC], const uint4 (&vr)[kUnroll][NC], int tb)
+                __attribute__((always_inline)) {
                 bool valid[kUnroll];
-                int pos[kUnroll];
 #pragma unroll
-                for (int u = 0; u < kUnroll; ++u) {
-                    const int idx = tb + u * TPI + tk;
-                    valid[u] = idx < len;
-                    const int li = valid[u] ? idx : tb;
-                    pos[u] = pos_lds[li];
-                    const int drow = spill ? row_lds[li] : pos[u];     // device row of the token
-                    int vo = lane_off, so = 0;
-                    if constexpr (TPI == 1) so = wave_uniform(drow) * row_stride;
-                    else vo += drow * row_stride;
-#pragma unroll
-                    for (int c = 0; c < NC; ++c) {
-                        kr[u][c] = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(rk, vo + c * 128, so, kStreamPolicy));
-                        vr[u][c] = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(rv, vo + c * 128, so, kStreamPolicy));
-                    }
-                }
+                for (int u = 0; u < kUnroll; ++u) valid[u] = tb + u * TPI + tk < len;
                 float xs[kUnroll][GS];
 #pragma unroll
                 for (int u = 0; u < kUnroll; ++u)
@@ -530,6 +582,31 @@ attention_kernel(AttnArgs a) {
                     if (done < (unsigned)wave_uniform((int)lead)) __builtin_amdgcn_s_setprio(2);
                     else __builtin_amdgcn_s_setprio(0);
                 }
+            };
+            int tb0 = wgrp * TT;
+            if constexpr (kPrefetch) {
+                if (have) {                       // rows requested with the staging loads
+                    tile(kp, vp, tb0);
+                    tb0 += kGroups * TT;
+                }
+            }
+            for (int tb = tb0; tb < len; tb += kGroups * TT) {
+                uint4 kr[kUnroll][NC], vr[kUnroll][NC];
+#pragma unroll
+                for (int u = 0; u < kUnroll; ++u) {
+                    const int idx = tb + u * TPI + tk;
+                    const int li = idx < len ? idx : tb;
+                    const int drow = spill ? row_lds[li] : pos_lds[li];     // device row of the token
+                    int vo = lane_off, so = 0;
+                    if constexpr (TPI == 1) so = wave_uniform(drow) * row_stride;
+                    else vo += drow * row_stride;
+#pragma unroll
+                    for (int c = 0; c < NC; ++c) {
+                        kr[u][c] = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(rk, vo + c * 128, so, kStreamPolicy));
+                        vr[u][c] = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(rv, vo + c * 128, so, kStreamPolicy));
+                    }
+                }
+                tile(kr, vr, tb);
             }
             __builtin_amdgcn_s_setprio(0);
             __syncthreads();
@@ -736,6 +813,7 @@ attention_kernel(AttnArgs a) {
             }
         }
         }
+        first_piece = false;
         x = sb + i1;
     }
 }
@@ -818,6 +896,52 @@ finish_kernel(FinishArgs a, int D) {
     }
 }
 
+// First-tile records of every range of the attention grid, one workgroup per
+// state layer, one thread per range: the same split, the same piece and chunk
+// as the attention kernel takes (which compares the record with its own before
+// using it).
+__global__ void __launch_bounds__(256) plan_kernel(PlanArgs a) {
+    __shared__ int32_t seq_off[kMaxBatch + 1];
+    const size_t st = blockIdx.x;
+    plan_ranges(a.n_active + st * a.B, a.B, seq_off);
+    __syncthreads();
+    const int T = seq_off[a.B];
+    const int Gn = active_groups(T, a.grid);
+    const int32_t* list = a.list + st * a.B * a.cap;
+    for (int w = threadIdx.x; w < a.grid; w += blockDim.x) {
+        int32_t* rec = a.plan + (st * a.grid + w) * kPlanInts;
+        int b = -1, i0 = 0, len = 0;
+        const int x = (int)((int64_t)w * T / Gn);
+        const int x_end = (int)((int64_t)(w + 1) * T / Gn);
+        if (w < Gn && x < x_end) {
+            int lo = 0, hi = a.B - 1;              // last sequence with seq_off <= x
+            while (lo < hi) {
+                const int mid = (lo + hi + 1) >> 1;
+                if (seq_off[mid] <= x) lo = mid; else hi = mid - 1;
+            }
+            while (seq_off[lo + 1] <= x) ++lo;     // past empty lists (seq_off[B] = T > x)
+            const int sb = seq_off[lo] + kSeqCost, se = seq_off[lo + 1];
+            if (x_end > sb) {
+                b = lo;
+                i0 = max(x, sb) - sb;
+                len = min(kChunk, min(se, x_end) - sb - i0);
+            }
+        }
+        rec[0] = b;
+        rec[1] = i0;
+        rec[2] = len;
+        rec[3] = 0;
+        if (b >= 0) {
+            const int32_t* src = list + (size_t)b * a.cap + i0;
+            int v[kPlanTokens];
+#pragma unroll
+            for (int k = 0; k < kPlanTokens; ++k) v[k] = src[min(k, len - 1)];
+#pragma unroll
+            for (int k = 0; k < kPlanTokens; ++k) rec[4 + k] = v[k];
+        }
+    }
+}
+
 template <bool BF16, int D, int G>
 constexpr int state_floats() { return 2 * G + G * Row<BF16, D>::kPerLane; }
 
@@ -842,8 +966,18 @@ struct Launch {
 template <bool BF16, int D, int G, int HKV>
 hipError_t launch_t(const AttnArgs& a, const Launch& l) {
     const size_t lds = lds_bytes<BF16, D, G>(a);
-    auto k = attention_kernel<BF16, D, G, HKV>;
-    if (l.occ) return hipOccupancyMaxActiveBlocksPerMultiprocessor(l.occ, k, 64 * kWaves, lds);
+    constexpr bool kPF = prefetch_shape<BF16, D, G, HKV>();
+    if (l.occ) {                          // the variant that fits fewer workgroups
+        hipError_t e = hipOccupancyMaxActiveBlocksPerMultiprocessor(
+            l.occ, attention_kernel<BF16, D, G, HKV, false>, 64 * kWaves, lds);
+        if (e != hipSuccess || !kPF) return e;
+        int occ_pf = 0;
+        e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&occ_pf, attention_kernel<BF16, D, G, HKV, kPF>,
+                                                         64 * kWaves, lds);
+        if (occ_pf < *l.occ) *l.occ = occ_pf;
+        return e;
+    }
+    auto k = kPF && a.plan ? attention_kernel<BF16, D, G, HKV, kPF> : attention_kernel<BF16, D, G, HKV, false>;
     AttnArgs arg = a;
     void* args[] = {&arg};
     return hipExtLaunchKernel(reinterpret_cast<const void*>(k), dim3(l.grid), dim3(64 * kWaves),
@@ -936,6 +1070,12 @@ hipError_t launch_attention(const AttnArgs& a, int dtype_bf16, int head_dim, int
 hipError_t attention_occupancy(const AttnArgs& a, int dtype_bf16, int head_dim, int group,
                                int* blocks_per_cu) {
     return dispatch(a, dtype_bf16, head_dim, group, Launch{0, nullptr, nullptr, nullptr, blocks_per_cu});
+}
+
+hipError_t launch_plan(const PlanArgs& a, int n_states, hipStream_t s) {
+    if (a.B < 1 || a.B > kMaxBatch || a.grid < 1 || n_states < 1) return hipErrorInvalidValue;
+    hipLaunchKernelGGL(plan_kernel, dim3(n_states), dim3(256), 0, s, a);
+    return hipGetLastError();
 }
 
 hipError_t launch_finish(const FinishArgs& a, int head_dim, int slots_per_seq, hipStream_t s) {

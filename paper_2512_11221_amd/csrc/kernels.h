@@ -77,6 +77,26 @@ struct AttnArgs {
     int32_t first_layer;      // token scope: this launch starts the per-token sums
     float* rel_acc;           // token scope, [B][cap]: sum over layers and heads of the relevance
     float* xlog;              // softmax relevance, [B][cap][Hq]: q.k * log2(e)/sqrt(D) per listed token
+    const int32_t* plan;      // state base, [grid][kPlanInts] first-tile records of the ranges
+                              // (plan_kernel), or null
+};
+
+// The first positions of every attention range, staged after each list
+// rebuild, so that an attention workgroup can request its first K/V rows
+// before its chunk's positions and q arrive.  Record of range w:
+//   [0] sequence of the range's first piece, -1: the range has no real token
+//   [1] the piece's first list index  [2] its first chunk's length  [3] unused
+//   [4 .. 4 + kPlanTokens) list entries from the first list index on (the
+//   last entry of the chunk repeated past its end)
+constexpr int kPlanTokens = 32;
+constexpr int kPlanInts = 4 + kPlanTokens;
+constexpr int kPlanMinLayers = 4;   // fewer layers per step: no records (the launch costs more)
+
+struct PlanArgs {
+    const int32_t* list;      // [states][B][cap]
+    const int32_t* n_active;  // [states][B]
+    int32_t* plan;            // [states][grid][kPlanInts]
+    int32_t B, cap, grid;
 };
 
 // Per layer, after the attention: the split combine of Eq. 1.
@@ -218,6 +238,8 @@ hipError_t attention_occupancy(const AttnArgs& a, int dtype_bf16, int head_dim, 
 // slots_per_seq: about how many partial slots a sequence has (grid / B + 1).
 hipError_t launch_finish(const FinishArgs& a, int head_dim, int slots_per_seq, hipStream_t s);
 hipError_t launch_compact(const CompactArgs& a, int n_instances, hipStream_t s);
+// The first-tile records of every (state layer, range) after a list rebuild.
+hipError_t launch_plan(const PlanArgs& a, int n_states, hipStream_t s);
 // Segments per instance (and their length) for the rebuild; 1 = one workgroup per instance.
 int compact_segments(int n_instances, int cap, int* seg_len);
 hipError_t launch_weight_relevance(const RelevanceArgs& a, hipStream_t s);

@@ -115,6 +115,8 @@ struct asrkf_ctx {
     float* part_acc = nullptr;
     float* part_ml = nullptr;
     int32_t* slot_info = nullptr;   // [2B]: first slot, end slot per sequence
+    int32_t* plan = nullptr;        // [state_layers][grid][kPlanInts] first-tile records of the
+                                    // attention ranges (resident mode, several layers), or null
     float* ent_partial = nullptr;   // [B][kEntropySplitMax][3]
     int32_t* ent_ticket = nullptr;  // [B]
     unsigned long long* counters = nullptr;   // [0] listed_total, [1..3] recoveries, [5] rr,
@@ -229,7 +231,7 @@ void free_all(asrkf_ctx* ctx) {
                     ctx->counters, ctx->row_of, ctx->on_host, ctx->list_row, ctx->last_row,
                     ctx->row_owner, ctx->hand, ctx->pop_buf, ctx->out_pos, ctx->out_row, ctx->n_out, ctx->in_pos, ctx->in_row,
                     ctx->n_in, ctx->flags, ctx->t_dev, ctx->hmask, ctx->hlast, ctx->rel_acc, ctx->xlog,
-                    ctx->norm, ctx->seg_count};
+                    ctx->norm, ctx->seg_count, ctx->plan};
     for (void* p : ptrs) if (p) (void)hipFree(p);
     void* host[] = {ctx->khost, ctx->vhost, ctx->flags_host};
     for (void* p : host) if (p) (void)hipHostFree(p);
@@ -420,6 +422,10 @@ asrkf_status asrkf_init(const asrkf_config* cfg, asrkf_ctx** out) {
     ALLOC(part_acc, (size_t)ctx->n_slots * c.n_q_heads * c.head_dim * 4);
     ALLOC(part_ml, (size_t)ctx->n_slots * c.n_q_heads * 2 * 4);
     ALLOC(slot_info, (size_t)c.batch * 2 * 4);
+    // The first-tile records cost a launch per step and save about a memory round
+    // trip per attention launch: worth it from a few layers on.
+    if (!ctx->spill && c.n_layers >= kPlanMinLayers)
+        ALLOC(plan, (size_t)ctx->state_layers * ctx->grid * kPlanInts * 4);
     ALLOC(ent_partial, (size_t)c.batch * kEntropySplitMax * 3 * 4);
     ALLOC(ent_ticket, (size_t)c.batch * 4);
     ALLOC(counters, kCounters * sizeof(unsigned long long));
@@ -613,7 +619,19 @@ asrkf_status build_lists(asrkf_ctx* ctx, int forced_level, hipStream_t s) {
         a.xfer = ctx->counters + 8;
     }
     HIP_OK(ctx, launch_compact(a, n_inst, s));
-    if (!ctx->spill) return ASRKF_OK;
+    if (!ctx->spill) {
+        if (ctx->plan) {
+            PlanArgs p{};
+            p.list = ctx->list;
+            p.n_active = ctx->n_active;
+            p.plan = ctx->plan;
+            p.B = ctx->cfg.batch;
+            p.cap = ctx->cap;
+            p.grid = ctx->grid;
+            HIP_OK(ctx, launch_plan(p, ctx->state_layers, s));
+        }
+        return ASRKF_OK;
+    }
 
     // the flag tells the host (one step late, without a wait) that rows ran out
     HIP_OK(ctx, hipMemcpyAsync(ctx->flags_host, ctx->flags, 8, hipMemcpyDeviceToHost, s));
@@ -765,6 +783,7 @@ asrkf_status decode_step_impl(asrkf_ctx* ctx, int32_t layer, const void* q, cons
     a.part_ml = ctx->part_ml;
     a.slot_first = ctx->slot_info;
     a.slot_end = ctx->slot_info + c.batch;
+    a.plan = ctx->plan ? ctx->plan + (ctx->token_scope ? 0 : (size_t)layer) * ctx->grid * kPlanInts : nullptr;
     if (use_static) {
         float* base = static_cast<float*>(ctx->static_scratch);
         a.part_acc = base;

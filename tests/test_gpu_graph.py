@@ -81,10 +81,18 @@ def _capture(torch, A, ctx, w, buf):
     return g
 
 
-def test_captured_step_replays_like_eager_steps():
+# two layers; four layers with some 10k tokens per layer, where the
+# first-tile records are built inside the captured restore and used by the
+# captured attention launches
+_REPLAYED = [dict(), dict(name="graph-hh-records", n_layers=4, batch=4, prefill=[2600, 2400, 2800, 2300],
+                          f_hh=[0.35, 0.25, 0.3, 0.2], steps=20)]
+
+
+@pytest.mark.parametrize("case", range(len(_REPLAYED)))
+def test_captured_step_replays_like_eager_steps(case):
     import torch
     import paper_2512_11221_amd as A
-    w = _workload()
+    w = _workload(**_REPLAYED[case])
     s_cold, s_hot = gen.hh_relevance_bounds(w)
     assert s_cold < w.tau - H.MARGIN and s_hot > w.tau + H.MARGIN
     inst = [(l, b) for l in range(w.n_layers) for b in range(w.batch)]
