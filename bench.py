@@ -162,8 +162,11 @@ def metadata_bytes(w, W, K, attended, algo_bytes, traffic, roofline):
     upper bound: count read and write plus U write for every attended token),
     the compaction's scan of U over every position, q, out and the appended row
     of every (layer, sequence), and the split-K partials (written by attention,
-    read by the combine; one workgroup per CU plus one slot per sequence).  The
-    attention kernel's measured counter excess is given beside it."""
+    read by the combine; one workgroup per CU plus one slot per sequence), and
+    the first-tile records of the attention ranges (resident mode, four or more
+    layers: 32 list entries read and a 144-byte record written per range and
+    state layer, the record read back by the attention launch).  The attention
+    kernel's measured counter excess is given beside it."""
     import torch
     L, B, Hq, D = w.n_layers, w.batch, w.n_q_heads, w.head_dim
     esz = 2 if w.dtype == "bf16" else 4
@@ -176,6 +179,9 @@ def metadata_bytes(w, W, K, attended, algo_bytes, traffic, roofline):
         "q_out_append": K * L * B * (Hq * D * esz + Hq * D * 4 + w.kv_bytes_per_token()),
         "split_partials": 2 * K * L * (cus + B) * Hq * (D + 2) * 4,
     }
+    if w.spill_min_D == 0 and L >= 4:
+        state_layers = 1 if w.scope == "token" else L
+        parts["first_tile_records"] = K * state_layers * cus * (32 * 4 + 2 * 144)
     total = sum(parts.values())
     out = {"bytes_timed_steps": parts, "total": total, "fraction_of_algorithmic": total / algo_bytes}
     if traffic:
