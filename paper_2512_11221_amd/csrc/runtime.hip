@@ -9,6 +9,8 @@
 //   active list     [L][B][cap]           int32   ascending positions for the step
 //   n_active        [L][B]                int32
 //   partials        [grid+B][Hq][D+2]     fp32    split-K attention partials
+//   plan records    [L][grid][36]         int32   first tile of every attention range
+//                                                 (resident mode, four or more layers)
 //   per sequence    prompt length, escalation, level, entropy, p_max
 //   duration table  [max_ctx + 2]         int32   d(c) of Eq. 3, built exactly on the host
 // Spill mode adds, per (layer, sequence): the device row of every position,
