@@ -85,3 +85,17 @@ def test_wide_query_groups(tau):
                      steps=20, window_K=16, tau=tau, k_soft=1.0, vocab=64, logit_sigma=1.0,
                      recipe="gauss")
     _parity(w, H.Inputs(w))
+
+
+@pytest.mark.parametrize("layout", [
+    dict(n_q_heads=16, n_kv_heads=8, head_dim=128, dtype="f32"),    # 512 B head rows: 2 tokens per wave tile
+    dict(n_q_heads=32, n_kv_heads=8, head_dim=64, dtype="bf16"),    # 128 B head rows
+    dict(n_q_heads=16, n_kv_heads=8, head_dim=256, dtype="bf16"),   # 512 B head rows, G = 2
+])
+def test_other_row_sizes(layout):
+    """The other row sizes with one token per wave iteration: the tile holds 2
+    or 4 tokens per wave, so each wave takes a different part of the record."""
+    w = gen.Workload(name="plan-rows", seed=gen.SEED + 105, n_layers=4, batch=3,
+                     prefill=[3100, 2800, 3300], steps=12, window_K=16, tau=-math.inf, k_soft=1.0,
+                     vocab=64, logit_sigma=1.0, recipe="gauss", **layout)
+    _parity(w, H.Inputs(w))
